@@ -1,0 +1,269 @@
+#!/usr/bin/env python3
+"""Benchmark of the MT-DAO hot path on one MI355X.
+
+One step = one pass of the whole hot path over one batch of synthetic
+gradients: the per-replica clip norm (when the workload clips), the fused
+local step of every replica, and the replica-mean of every state the
+schedule makes due at that step.  Inputs (states and one filled gradient
+buffer) are resident in HBM before the timed region.  The default run times
+256 consecutive steps of the 1.31B-parameter, K=4, Adam N=3 fp32 workload,
+so the timed window holds exactly the amortised share of syncs (x: 4,
+each u^j: 2, v: 1).
+
+Prints ONE JSON line.  Extra objects:
+  step / sync       element-updates/s and GB/s of each part, % of HBM peak
+  roofline          dominant kernel (the local step): algorithmic bytes per
+                    launch / mean launch time from HIP events on its stream
+  cpu_baseline      the CPU oracle on a bounded sample of the same workload
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "param-element updates/s (x K workers) + achieved HBM GB/s % peak, step & sync"
+HBM_PEAK_GBS = 8000.0
+DEFAULT_WORKLOAD = "adam_n3_k4_p1311m"
+KERNEL_SRC = os.path.join(ROOT, "paper_2510_05361_amd", "csrc", "kernels.hpp")
+
+
+def step_bytes_per_element(w) -> int:
+    """Algorithmic HBM bytes of one element-update of the local step: read
+    and write x, u^1..u^N, v; read g (plus one more read of g for the
+    clip norm)."""
+    p = 2 if w.param_dtype == "bf16" else 4
+    pg = 2 if w.grad_dtype == "bf16" else 4
+    b = 2 * p + pg + 8 * w.n_moments + (8 if w.has_v else 0)
+    return b
+
+
+def norm_bytes_per_element(w) -> int:
+    if w.clip_rho > 0 and w.form != "adopt":
+        return 2 if w.grad_dtype == "bf16" else 4
+    return 0
+
+
+def kernel_hash() -> str:
+    with open(KERNEL_SRC, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def load_traffic(workload: str, launch_bytes: float):
+    """HBM traffic of the local-step kernel from committed rocprofv3 --pmc
+    counters (FETCH_SIZE and WRITE_SIZE per dispatch, scaled by the same
+    counters' reading for a plain copy of known size); None when absent or
+    taken on another version of the kernel source."""
+    path = os.path.join(ROOT, "profiles", f"traffic_k_local_step_{workload}.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        t = json.load(f)
+    if t.get("kernel_source_sha256_16") != kernel_hash():
+        return None
+    return float(t["traffic_bytes_per_launch"])
+
+
+def cpu_baseline(w, target_s: float = 12.0):
+    """The CPU oracle, as it is, single-threaded, on a sample of the same
+    workload: a slice of 2^20 elements per replica (every replica), timed
+    for local steps until ~target_s of work, plus one replica mean of one
+    state on the slice; the sync cost is amortised by the schedule."""
+    import numpy as np
+
+    import oracle
+    import synth
+
+    n = min(w.numel, 1 << 20)
+    idx = np.arange(n, dtype=np.int64)
+    cfg = oracle.OracleConfig.from_workload(w)
+    st = oracle.new_state(cfg, synth.host_x0_row(w, idx), w.replicas)
+    g = synth.host_grad_rows(w, 1, idx)
+    scale = np.ones(w.replicas) if w.clip_rho > 0 and w.form != "adopt" else None
+    steps, t0 = 0, time.perf_counter()
+    while True:
+        s = steps + 2
+        if scale is not None:
+            for m in range(w.replicas):
+                oracle.sumsq(g[m], w.grad_dtype)
+        oracle.local_step(cfg, st, g, s, w.lr, w.adopt_clip_value(s), scale)
+        steps += 1
+        el = time.perf_counter() - t0
+        if el >= target_s or steps >= 1000:
+            break
+    t_step = el / steps
+    t1 = time.perf_counter()
+    oracle.replica_mean(st.u[0], "f32")
+    t_mean = time.perf_counter() - t1
+    syncs_per_step = (1.0 / w.period_x if w.period_x else 0.0) + sum(
+        1.0 / h for h in w.period_u if h) + (1.0 / w.period_v if (w.has_v and w.period_v) else 0.0)
+    t = t_step + syncs_per_step * t_mean
+    return {
+        "value": w.replicas * n / t,
+        "unit": "element-updates/s",
+        "cores": 1,
+        "kind": "oracle",
+        "sample": (f"{n} elements x {w.replicas} replicas of {w.name}: {steps} local steps "
+                   f"({el:.1f} s, clip norms included) + one replica mean, sync amortised "
+                   f"at {syncs_per_step:.4f} state-syncs/step; single thread"),
+    }
+
+
+def calibrate_copy(nbytes: int, reps: int) -> None:
+    """A plain device copy of known size (torch's copy kernel): the
+    reference reading of FETCH_SIZE / WRITE_SIZE under rocprofv3 --pmc."""
+    import torch
+
+    n = nbytes // 4
+    a = torch.ones(n, dtype=torch.float32, device="cuda:0")
+    b = torch.empty_like(a)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    dt = (time.perf_counter() - t0) / reps
+    print(json.dumps({"copy_bytes_each_way": n * 4, "reps": reps, "ms": dt * 1e3,
+                      "GBps_read_plus_write": 2 * n * 4 / dt / 1e9}), flush=True)
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=256)
+    ap.add_argument("--warmup", type=int, default=8)
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES",
+                    help="only run a plain copy of BYTES each way (counter calibration)")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported (the path is built "
+              "and measured on a single MI355X; see the sharding notes of the design)", file=sys.stderr)
+        return 2
+
+    if args.calibrate_copy:
+        calibrate_copy(args.calibrate_copy, max(1, args.steps))
+        return 0
+
+    import torch
+
+    import synth
+    from paper_2510_05361_amd import mtdao as abi
+    from paper_2510_05361_amd.optimizer import MtdaoOptimizer
+    from synth.device import DeviceInputs
+
+    w = synth.WORKLOADS[args.workload]
+    d = torch.device("cuda:0")
+    K, P = w.replicas, w.numel
+    print(f"bench: {w.name} K={K} P={P} warmup={args.warmup} steps={args.steps}", file=sys.stderr,
+          flush=True)
+    dev = DeviceInputs(w, d)
+    cfg = abi.config_from_workload(w)
+    opt = MtdaoOptimizer(cfg, d, x0=dev.x0_row())
+    gdt = torch.bfloat16 if w.grad_dtype == "bf16" else torch.float32
+    grads = torch.empty((K, P), dtype=gdt, device=d)
+    dev.grads_into(1, grads)
+    del dev
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+
+    def one_step(s, ev=None):
+        if ev is not None:
+            ev[0].record(stream)
+        opt.step(grads, w.lr, w.adopt_clip_value(s))
+        if ev is not None:
+            ev[1].record(stream)
+        return opt.sync()
+
+    s = 0
+    for _ in range(args.warmup):
+        s += 1
+        one_step(s)
+    torch.cuda.synchronize()
+
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(args.steps)]
+    syncs = {}
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        s += 1
+        applied = one_step(s, evs[k])
+        if applied:
+            syncs[s] = applied
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    step_ms = [a.elapsed_time(b) for a, b in evs]
+    step_launch_s = sum(step_ms) / len(step_ms) / 1e3
+
+    # per-state sync time (replica mean of one state), untimed region
+    nstates = 1 + w.n_moments + (1 if w.has_v else 0)
+    sync_s = []
+    for sid in range(nstates):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        opt.sync(1 << sid)
+        a.record(stream)
+        reps = 5
+        for _ in range(reps):
+            opt.sync(1 << sid)
+        b.record(stream)
+        torch.cuda.synchronize()
+        sync_s.append(a.elapsed_time(b) / reps / 1e3)
+    opt.close()
+
+    eb = step_bytes_per_element(w) + norm_bytes_per_element(w)
+    launch_bytes = K * P * step_bytes_per_element(w)
+    step_gbs = K * P * eb / step_launch_s / 1e9
+    sync_report = []
+    names = ["x"] + [f"u{j + 1}" for j in range(w.n_moments)] + (["v"] if w.has_v else [])
+    for sid, t in enumerate(sync_s):
+        es = 2 if (sid == 0 and w.param_dtype == "bf16") else 4
+        gbs = 2 * K * es * P / t / 1e9
+        sync_report.append({"state": names[sid], "ms": t * 1e3, "GBps": gbs, "pct_hbm_peak": 100 * gbs / HBM_PEAK_GBS})
+
+    value = K * P * args.steps / wall
+    traffic = load_traffic(w.name, launch_bytes)
+    out = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "element-updates/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": wall / args.steps * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32" if w.param_dtype == "f32" else "bf16 params, f32 moments",
+        "data": "synthetic (seeded gradients and parameters shaped like the paper's GPT tensor lists)",
+        "config": {"workload": w.name, "replicas": K, "params_per_replica": P, "form": w.form,
+                   "n_moments": w.n_moments, "param_dtype": w.param_dtype, "grad_dtype": w.grad_dtype,
+                   "periods": {"x": w.period_x, "u": list(w.period_u), "v": w.period_v},
+                   "syncs_in_window": {str(k): v for k, v in sorted(syncs.items())}},
+        "step": {"mean_launch_ms": step_launch_s * 1e3, "element_updates_per_s": K * P / step_launch_s,
+                 "bytes_per_element_update": eb, "GBps": step_gbs,
+                 "pct_hbm_peak": 100 * step_gbs / HBM_PEAK_GBS},
+        "sync": sync_report,
+        "roofline": {"bound": "hbm", "achieved": launch_bytes / step_launch_s / 1e9, "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": launch_bytes / step_launch_s / 1e9 / HBM_PEAK_GBS,
+                     "traffic": traffic, "kernel": "k_local_step",
+                     "algorithmic_bytes_per_launch": launch_bytes},
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(w)
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,190 @@
+/*
+ * mtdao.h -- C ABI of the MT-DAO optimizer hot path on MI355X (gfx950).
+ *
+ * MT-DAO ("Multi-timescale Distributed Adaptive Optimizers with Local
+ * Updates"): every worker m keeps its own parameters x^m, N first-moment
+ * EMAs u^{j,m} with their own decay rates beta_{1,j}, and (Adam and ADOPT
+ * forms) one second moment v^m.  A local step combines the current gradient
+ * and the N moments quasi-hyperbolically with weights (1 - sum_j omega_j)
+ * and omega_j (Section 2.3, Algorithm 1 = Adam form; Algorithm 2 = ADOPT
+ * form; Algorithm 3 = SGDM form).  Periodically each state is replaced by
+ * its mean over the workers, every state on its own period K_x, K_j, K_v
+ * (the "t mod K" conditions of the same algorithms, OuterOpt = averaging).
+ *
+ * On one GPU the M workers (called K "replicas" here) are K resident rows
+ * of every state buffer, and the averaging is an on-device mean over the
+ * replica axis.
+ *
+ * Memory layout (all device buffers are caller-owned, e.g. torch tensors):
+ *   x      [K][P]  params, fp32 or bf16 (row m = worker m)
+ *   u[j]   [K][P]  fp32, j = 0..N-1 (first moments, paper u^{j+1})
+ *   v      [K][P]  fp32 (Adam, ADOPT only; NULL for SGDM)
+ *   grads  [K][P]  fp32 or bf16, one gradient row per worker per step
+ * P is the total element count of one replica's flat multi-tensor buffer
+ * (all tensors of the model concatenated); every call covers all tensors of
+ * all replicas.  Rows are contiguous with stride P.  Every pointer must be
+ * 16-byte aligned.
+ *
+ * Step numbering: s counts local updates; the k-th call of
+ * mtdao_local_step performs update s = start_step + k (1-based).  State S is
+ * due for averaging after update s iff its period H_S > 0 and s mod H_S ==
+ * 0 (period 0 = never).  This is Algorithm 1's schedule; Algorithms 2 and 3
+ * print the same rule with a one-step phase difference for u and v, which
+ * is read as a slip (the unified strategy of the wall-clock appendix syncs
+ * parameters and all optimizer states together every K steps).
+ *
+ * Readings where the paper is silent (Algorithm 1's caption omits the bias
+ * correction; the clip types are not spelled out):
+ *   - Adam bias correction (bias_correction = 1): u_j / (1 - beta_{1,j}^s) and
+ *     v / (1 - beta_2^s) with the global s, never reset by averaging; the
+ *     gradient term is uncorrected.  ADOPT and SGDM have no correction.
+ *   - clip(g, rho): per-replica global L2 norm over all P elements,
+ *     scale = min(1, rho / ||g^m||), 1 when the norm is 0.  Adam's v squares
+ *     the clipped gradient.
+ *   - ADOPT clip(g_hat, c_t): element-wise clamp to [-c_t, c_t], c_t passed
+ *     per call.  adopt_order PREV normalises by v from before this step and
+ *     the first update (s == 1) only sets v = g^2 (ADOPT as published); CUR
+ *     normalises by the freshly updated v, literally as Algorithm 2 prints.
+ *
+ * Concurrency: calls on one handle must be serialised by the caller; all
+ * work is enqueued on the HIP stream passed to each call (NULL = the null
+ * stream).  mtdao_local_step and mtdao_sync only enqueue; mtdao_read_state
+ * waits for the stream.
+ *
+ * Errors: every int32_t-returning call returns MTDAO_OK (0) or a negative
+ * code; validation happens on the host before anything is enqueued, so a
+ * failing call leaves the device state untouched.  mtdao_last_error gives a
+ * human-readable message.
+ */
+#ifndef MTDAO_H
+#define MTDAO_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define MTDAO_MAX_N 4            /* max number of first moments N          */
+#define MTDAO_MAX_REPLICAS 1024  /* max K                                   */
+#define MTDAO_SYNC_AUTO 0xFFFFFFFFu
+
+/* forms: Algorithm 1 / Algorithm 2 / Algorithm 3 */
+enum { MTDAO_ADAM = 0, MTDAO_ADOPT = 1, MTDAO_SGDM = 2 };
+/* storage types of params and gradients (moments are always fp32) */
+enum { MTDAO_F32 = 0, MTDAO_BF16 = 1 };
+/* ADOPT normalisation order */
+enum { MTDAO_ADOPT_PREV = 0, MTDAO_ADOPT_CUR = 1 };
+/* status codes */
+enum {
+  MTDAO_OK = 0,
+  MTDAO_ERR_INVALID_ARG = -1, /* bad config value, NULL pointer, bad state id */
+  MTDAO_ERR_ALIGN = -2,       /* a device pointer is not 16-byte aligned     */
+  MTDAO_ERR_HIP = -3,         /* a HIP runtime call failed (message kept)     */
+  MTDAO_ERR_RANGE = -4,       /* offset/count/replica out of range           */
+  MTDAO_ERR_WORKSPACE = -5    /* workspace missing or smaller than required  */
+};
+
+/* Mask bits of mtdao_sync / mtdao_schedule: bit 0 = x, bit j (1..N) = u^j,
+ * bit N+1 = v.  State ids of mtdao_read_state use the same numbering. */
+
+/* Optimizer configuration: the Require block of Algorithms 1-3. */
+typedef struct mtdao_config {
+  int32_t form;             /* MTDAO_ADAM / MTDAO_ADOPT / MTDAO_SGDM               */
+  int32_t replicas;         /* K >= 1: workers (the paper's M)                       */
+  int32_t n_moments;        /* N, 1..MTDAO_MAX_N                                     */
+  int32_t param_dtype;      /* MTDAO_F32 / MTDAO_BF16 storage of x                   */
+  int32_t grad_dtype;       /* MTDAO_F32 / MTDAO_BF16 storage of the gradients       */
+  int32_t adopt_order;      /* MTDAO_ADOPT_PREV (default) / MTDAO_ADOPT_CUR          */
+  int32_t bias_correction;  /* Adam only: 1 = bias-correct u^j and v, 0 = none       */
+  float beta1[MTDAO_MAX_N]; /* beta_{1,j} in [0,1)                                   */
+  float omega[MTDAO_MAX_N]; /* omega_j in [0,1], sum <= 1 (+1e-6)                    */
+  float beta2;              /* beta_2 in [0,1) (Adam, ADOPT)                         */
+  float eps;                /* epsilon >= 0 (Adam, ADOPT)                            */
+  float clip_rho;           /* rho > 0: global-norm clip (Adam, SGDM); <= 0: off     */
+  int32_t period_x;         /* K_x >= 0 (0 = never)                                  */
+  int32_t period_u[MTDAO_MAX_N]; /* K_j >= 0                                         */
+  int32_t period_v;         /* K_v >= 0 (ignored by SGDM)                            */
+  int64_t start_step;       /* updates already applied (0 fresh; s for a resume)     */
+  int64_t numel;            /* P >= 0: elements per replica                          */
+  int32_t n_tensors;        /* entries of tensor_numel (0: one tensor of P elements) */
+  const int64_t* tensor_numel; /* host array, sums to P; copied by mtdao_init        */
+} mtdao_config;
+
+/* Device state buffers (caller-owned, [K][P] each, see layout above). */
+typedef struct mtdao_buffers {
+  void* x;                  /* params                                                */
+  float* u[MTDAO_MAX_N];    /* first moments u^1..u^N (entries >= N ignored)         */
+  float* v;                 /* second moment (NULL for SGDM)                         */
+  int32_t init_states;      /* 0: x row 0 is broadcast to all rows, u and v zeroed   */
+                            /* 1: all rows of x, u, v are kept as given (resume)     */
+} mtdao_buffers;
+
+typedef struct mtdao_handle mtdao_handle;
+
+/* Device workspace (bytes) that mtdao_init needs for this configuration:
+ * per-replica clip factors and the partial sums of the gradient-norm
+ * reduction (clip_rho > 0), 0 otherwise.  Host-only; no GPU needed. */
+int32_t mtdao_workspace_bytes(const mtdao_config* cfg, size_t* bytes);
+
+/* Validate cfg and build a handle over the caller's buffers.  With
+ * init_states == 0 it enqueues the broadcast of x_0 (row 0) to every
+ * replica and zero-fills u and v (the initial u_{-1} = v_{-1} = 0), as the
+ * Require block's single x_0 and the "initialize" line of Algorithms 1-3
+ * state.  workspace: device buffer of at least mtdao_workspace_bytes
+ * (may be NULL when that is 0), caller-owned, must outlive the handle.
+ * The handle is library-owned: release it with mtdao_destroy. */
+int32_t mtdao_init(const mtdao_config* cfg, const mtdao_buffers* bufs, void* workspace,
+                   size_t workspace_bytes, void* hip_stream, mtdao_handle** out);
+
+/* One local update of every replica (the body of Algorithms 1-3 for all
+ * workers in parallel): s += 1, then for every replica m and element i the
+ * form's update of u^j, v and x from grads[m][i].
+ *   grads       device [K][P] in cfg.grad_dtype, read only
+ *   lr          eta_t of this update
+ *   adopt_clip  ADOPT's c_t for this update (<= 0: no clamp); ignored otherwise
+ * With clip_rho > 0 it first reduces ||grads[m]||_2 per replica (one extra
+ * read of the gradient) in a fixed order, so results are deterministic. */
+int32_t mtdao_local_step(mtdao_handle* h, const void* grads, float lr, float adopt_clip,
+                         void* hip_stream);
+
+/* Replica averaging E_m[.] of the states selected by mask, after the last
+ * local update (step s = mtdao_step_count).  mask = MTDAO_SYNC_AUTO applies
+ * the schedule (states whose period divides s); any other value is taken as
+ * the explicit set of states to average (e.g. the Bernoulli draws of the
+ * probabilistic variant, Algorithm 4, made by the caller).  Every element of
+ * every selected state becomes S^0 + (sum_{m>=1} (S^m - S^0)) / K computed
+ * in fp32 and is written to all K rows, so averaging identical rows is an
+ * exact no-op and a repeated call at the same s changes nothing.
+ * applied_mask (may be NULL) receives the set actually averaged. */
+int32_t mtdao_sync(mtdao_handle* h, uint32_t mask, uint32_t* applied_mask, void* hip_stream);
+
+/* The schedule alone: states due after update s for this configuration.
+ * Host-only; no GPU needed. */
+int32_t mtdao_schedule(const mtdao_config* cfg, int64_t s, uint32_t* mask);
+
+/* Copy count elements of one state row to host memory and wait for it:
+ *   state    0 = x (cfg.param_dtype), 1..N = u^j, N+1 = v (fp32)
+ *   replica  0..K-1;  offset, count within [0, P]
+ *   host_dst caller-owned, count * element-size bytes
+ * Enqueued on hip_stream after earlier work; returns when the copy is done. */
+int32_t mtdao_read_state(mtdao_handle* h, int32_t state, int32_t replica, int64_t offset,
+                         int64_t count, void* host_dst, void* hip_stream);
+
+/* Number of local updates applied so far (start_step + calls). -1 for NULL. */
+int64_t mtdao_step_count(const mtdao_handle* h);
+
+/* Message of the last failing call on h; with h == NULL, of the last
+ * failing call that had no handle (init, workspace_bytes, schedule) on this
+ * thread.  Never NULL; "" when there was no error. */
+const char* mtdao_last_error(const mtdao_handle* h);
+
+/* Release the handle (never the caller's buffers).  NULL is a no-op. */
+void mtdao_destroy(mtdao_handle* h);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MTDAO_H */

@@ -1,0 +1,381 @@
+// Device kernels of the MT-DAO hot path for CDNA4 (gfx950).
+//
+// All kernels are streaming, HBM-bound passes: the local step reads x, g,
+// u^1..u^N, v once and writes x, u^1..u^N, v once per element (no MFMA:
+// there is no contraction).  Every thread owns V consecutive elements of
+// one replica row per vector slot, so loads and stores are 16-byte vector
+// accesses and a 64-lane wavefront moves 1 KiB per instruction; U slots
+// per thread are issued before any of them is consumed to keep enough
+// bytes in flight per CU.  Rows are replica-major [K][P]; blockIdx.y is
+// the replica (or the state, for the mean), blockIdx.x strides over tiles
+// of 256*V*U elements of the row.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace mtdao {
+
+constexpr int kBlock = 256;
+constexpr int kMaxN = 4;
+constexpr int kMaxMeanStates = 2 + kMaxN;
+
+enum Form { kAdam = 0, kAdopt = 1, kSgdm = 2 };
+enum AdoptOrder { kPrev = 0, kCur = 1 };
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint16_t u16x4 __attribute__((ext_vector_type(4)));
+typedef uint16_t u16x8 __attribute__((ext_vector_type(8)));
+
+// ------------------------------------------------------------ conversions
+
+__device__ __forceinline__ float bf16_to_f32(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
+
+// Round-to-nearest-even fp32 -> bf16 (NaN stays a quiet NaN).
+__device__ __forceinline__ uint16_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40u);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+// --------------------------------------------------- vector load / store
+//
+// load_v<T, V>(p, e, out): V consecutive elements starting at element e,
+// widened to fp32.  T = float, or uint16_t holding bf16 bit patterns.  V = 1 (scalar path for rows whose
+// length breaks 16-byte alignment), 4 or 8.
+
+template <bool NT, typename VT>
+__device__ __forceinline__ VT ld(const VT* p) {
+  if constexpr (NT) return __builtin_nontemporal_load(p);
+  else return *p;
+}
+
+template <bool NT, typename VT>
+__device__ __forceinline__ void st(VT* p, VT v) {
+  if constexpr (NT) __builtin_nontemporal_store(v, p);
+  else *p = v;
+}
+
+template <typename T, int V, bool NT>
+__device__ __forceinline__ void load_v(const T* __restrict__ p, int64_t e, float (&o)[V]) {
+  if constexpr (sizeof(T) == 4) {
+    const float* q = reinterpret_cast<const float*>(p) + e;
+    if constexpr (V == 1) {
+      o[0] = ld<NT>(q);
+    } else {
+#pragma unroll
+      for (int k = 0; k < V / 4; ++k) {
+        f32x4 a = ld<NT>(reinterpret_cast<const f32x4*>(q) + k);
+        o[4 * k + 0] = a.x; o[4 * k + 1] = a.y; o[4 * k + 2] = a.z; o[4 * k + 3] = a.w;
+      }
+    }
+  } else {
+    const uint16_t* q = reinterpret_cast<const uint16_t*>(p) + e;
+    if constexpr (V == 1) {
+      o[0] = bf16_to_f32(ld<NT>(q));
+    } else if constexpr (V == 4) {
+      u16x4 a = ld<NT>(reinterpret_cast<const u16x4*>(q));
+#pragma unroll
+      for (int k = 0; k < 4; ++k) o[k] = bf16_to_f32(a[k]);
+    } else {
+#pragma unroll
+      for (int k = 0; k < V / 8; ++k) {
+        u16x8 a = ld<NT>(reinterpret_cast<const u16x8*>(q) + k);
+#pragma unroll
+        for (int t = 0; t < 8; ++t) o[8 * k + t] = bf16_to_f32(a[t]);
+      }
+    }
+  }
+}
+
+template <typename T, int V, bool NT>
+__device__ __forceinline__ void store_v(T* __restrict__ p, int64_t e, const float (&o)[V]) {
+  if constexpr (sizeof(T) == 4) {
+    float* q = reinterpret_cast<float*>(p) + e;
+    if constexpr (V == 1) {
+      st<NT>(q, o[0]);
+    } else {
+#pragma unroll
+      for (int k = 0; k < V / 4; ++k) {
+        f32x4 a = {o[4 * k + 0], o[4 * k + 1], o[4 * k + 2], o[4 * k + 3]};
+        st<NT>(reinterpret_cast<f32x4*>(q) + k, a);
+      }
+    }
+  } else {
+    uint16_t* q = reinterpret_cast<uint16_t*>(p) + e;
+    if constexpr (V == 1) {
+      st<NT>(q, f32_to_bf16(o[0]));
+    } else if constexpr (V == 4) {
+      u16x4 a;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) a[k] = f32_to_bf16(o[k]);
+      st<NT>(reinterpret_cast<u16x4*>(q), a);
+    } else {
+#pragma unroll
+      for (int k = 0; k < V / 8; ++k) {
+        u16x8 a;
+#pragma unroll
+        for (int t = 0; t < 8; ++t) a[t] = f32_to_bf16(o[8 * k + t]);
+        st<NT>(reinterpret_cast<u16x8*>(q) + k, a);
+      }
+    }
+  }
+}
+
+// ------------------------------------------------------------ local step
+
+// Per-launch scalars, prepared on the host in double and rounded to fp32.
+struct StepParams {
+  void* x;                 // [K][P] params (XT)
+  const void* g;           // [K][P] gradients (GT)
+  float* u[kMaxN];         // [K][P] first moments
+  float* v;                // [K][P] second moment (Adam, ADOPT)
+  const float* scale;      // [K] global-norm clip factors, or nullptr
+  int64_t P;               // row length
+  int64_t tiles;           // ceil(P / (kBlock * V * U))
+  float beta[kMaxN];       // beta_{1,j}
+  float omb[kMaxN];        // 1 - beta_{1,j}
+  float w[kMaxN];          // omega_j (times 1/(1 - beta_{1,j}^s) for bias-corrected Adam)
+  float gw;                // 1 - sum_j omega_j: weight of the current gradient
+  float beta2, omb2;       // beta_2, 1 - beta_2
+  float inv_bc2;           // 1/(1 - beta_2^s) (Adam with bias correction), else 1
+  float eps;
+  float lr;                // eta_t
+  float clip;              // ADOPT c_t (<= 0: no clamp)
+};
+
+// One update of all elements of all replicas (Algorithm 1, 2 or 3 body).
+//   FORM       kAdam / kAdopt / kSgdm
+//   N          number of first moments
+//   XT, GT     storage of params / gradients (float or bf16)
+//   V, U       elements per vector slot, slots per thread per tile
+//   ORDER      ADOPT normalisation order (kPrev: v from before this step)
+template <int FORM, int N, typename XT, typename GT, int V, int U, bool NT, int ORDER>
+__global__ __launch_bounds__(kBlock) void k_local_step(StepParams p) {
+  const int64_t m = blockIdx.y;
+  const int64_t row = m * p.P;
+  XT* __restrict__ x = reinterpret_cast<XT*>(p.x) + row;
+  const GT* __restrict__ g = reinterpret_cast<const GT*>(p.g) + row;
+  float* __restrict__ u[N];
+#pragma unroll
+  for (int j = 0; j < N; ++j) u[j] = p.u[j] + row;
+  float* __restrict__ v = (FORM == kSgdm) ? nullptr : p.v + row;
+  const float sc = (FORM != kAdopt && p.scale != nullptr) ? p.scale[m] : 1.0f;
+
+  for (int64_t tile = blockIdx.x; tile < p.tiles; tile += gridDim.x) {
+    const int64_t base = tile * (int64_t)(kBlock * V * U);
+    float gv[U][V], xv[U][V], uv[U][N][V], vv[U][V];
+    // issue every load of the tile before any arithmetic
+#pragma unroll
+    for (int k = 0; k < U; ++k) {
+      const int64_t e = base + ((int64_t)k * kBlock + threadIdx.x) * V;
+      if (e < p.P) {
+        load_v<GT, V, NT>(g, e, gv[k]);
+        load_v<XT, V, NT>(x, e, xv[k]);
+#pragma unroll
+        for (int j = 0; j < N; ++j) load_v<float, V, NT>(u[j], e, uv[k][j]);
+        if constexpr (FORM != kSgdm) load_v<float, V, NT>(v, e, vv[k]);
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < U; ++k) {
+      const int64_t e = base + ((int64_t)k * kBlock + threadIdx.x) * V;
+      if (e >= p.P) continue;
+#pragma unroll
+      for (int t = 0; t < V; ++t) {
+        const float graw = gv[k][t];
+        if constexpr (FORM == kAdam) {
+          const float gh = sc * graw;
+          float num = p.gw * gh;
+#pragma unroll
+          for (int j = 0; j < N; ++j) {
+            const float uj = p.beta[j] * uv[k][j][t] + p.omb[j] * gh;
+            uv[k][j][t] = uj;
+            num += p.w[j] * uj;
+          }
+          const float vn = p.beta2 * vv[k][t] + p.omb2 * (gh * gh);
+          vv[k][t] = vn;
+          const float den = __builtin_sqrtf(vn * p.inv_bc2) + p.eps;
+          xv[k][t] = xv[k][t] - p.lr * (num / den);
+        } else if constexpr (FORM == kAdopt) {
+          float gn;
+          if constexpr (ORDER == kPrev) {
+            gn = graw / (__builtin_sqrtf(vv[k][t]) + p.eps);
+            vv[k][t] = p.beta2 * vv[k][t] + p.omb2 * (graw * graw);
+          } else {
+            vv[k][t] = p.beta2 * vv[k][t] + p.omb2 * (graw * graw);
+            gn = graw / (__builtin_sqrtf(vv[k][t]) + p.eps);
+          }
+          if (p.clip > 0.0f) gn = gn > p.clip ? p.clip : (gn < -p.clip ? -p.clip : gn);
+          float delta = p.gw * gn;
+#pragma unroll
+          for (int j = 0; j < N; ++j) {
+            const float uj = p.beta[j] * uv[k][j][t] + p.omb[j] * gn;
+            uv[k][j][t] = uj;
+            delta += p.w[j] * uj;
+          }
+          xv[k][t] = xv[k][t] - p.lr * delta;
+        } else {
+          const float gh = sc * graw;
+          float delta = p.gw * gh;
+#pragma unroll
+          for (int j = 0; j < N; ++j) {
+            const float uj = p.beta[j] * uv[k][j][t] + p.omb[j] * gh;
+            uv[k][j][t] = uj;
+            delta += p.w[j] * uj;
+          }
+          xv[k][t] = xv[k][t] - p.lr * delta;
+        }
+      }
+      store_v<XT, V, NT>(x, e, xv[k]);
+#pragma unroll
+      for (int j = 0; j < N; ++j) store_v<float, V, NT>(u[j], e, uv[k][j]);
+      if constexpr (FORM != kSgdm) store_v<float, V, NT>(v, e, vv[k]);
+    }
+  }
+}
+
+// ADOPT's first update with the previous-v order: v = g^2, nothing else.
+template <typename GT, int V, int U, bool NT>
+__global__ __launch_bounds__(kBlock) void k_adopt_init_v(const void* gp, float* vp, int64_t P, int64_t tiles) {
+  const int64_t row = (int64_t)blockIdx.y * P;
+  const GT* __restrict__ g = reinterpret_cast<const GT*>(gp) + row;
+  float* __restrict__ v = vp + row;
+  for (int64_t tile = blockIdx.x; tile < tiles; tile += gridDim.x) {
+    const int64_t base = tile * (int64_t)(kBlock * V * U);
+#pragma unroll
+    for (int k = 0; k < U; ++k) {
+      const int64_t e = base + ((int64_t)k * kBlock + threadIdx.x) * V;
+      if (e >= P) continue;
+      float a[V];
+      load_v<GT, V, NT>(g, e, a);
+#pragma unroll
+      for (int t = 0; t < V; ++t) a[t] = a[t] * a[t];
+      store_v<float, V, NT>(v, e, a);
+    }
+  }
+}
+
+// --------------------------------------------------------- replica mean
+
+struct MeanParams {
+  void* state[kMaxMeanStates];  // [K][P] buffers of one storage type
+  int64_t P;
+  int64_t tiles;
+  int32_t K;
+};
+
+// E_m[S] for the state blockIdx.y: every element becomes
+// S^0 + (sum_{m>=1} (S^m - S^0)) / K in fp32 and is stored to all K rows.
+// Each thread reads the K rows of its own columns and writes them back, so
+// the in-place update has no cross-thread hazard.
+template <typename T, int V, bool NT>
+__global__ __launch_bounds__(kBlock) void k_replica_mean(MeanParams p) {
+  T* __restrict__ s = reinterpret_cast<T*>(p.state[blockIdx.y]);
+  const float kf = (float)p.K;
+  for (int64_t tile = blockIdx.x; tile < p.tiles; tile += gridDim.x) {
+    const int64_t e = tile * (int64_t)(kBlock * V) + (int64_t)threadIdx.x * V;
+    if (e >= p.P) continue;
+    float s0[V], d[V];
+    load_v<T, V, NT>(s, e, s0);
+#pragma unroll
+    for (int t = 0; t < V; ++t) d[t] = 0.0f;
+#pragma unroll 4
+    for (int32_t m = 1; m < p.K; ++m) {
+      float a[V];
+      load_v<T, V, NT>(s + (int64_t)m * p.P, e, a);
+#pragma unroll
+      for (int t = 0; t < V; ++t) d[t] += a[t] - s0[t];
+    }
+#pragma unroll
+    for (int t = 0; t < V; ++t) s0[t] = s0[t] + d[t] / kf;
+#pragma unroll 4
+    for (int32_t m = 0; m < p.K; ++m) store_v<T, V, NT>(s + (int64_t)m * p.P, e, s0);
+  }
+}
+
+// ----------------------------------------------------- global-norm clip
+
+__device__ __forceinline__ double wave_sum(double a) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) a += __shfl_xor(a, o, 64);
+  return a;
+}
+
+// Partial sums of g^2 in fp64 for replica blockIdx.y; each block writes
+// one partial (fixed order: deterministic for a fixed grid).
+template <typename GT, int V, int U>
+__global__ __launch_bounds__(kBlock) void k_sumsq_partial(const void* gp, int64_t P, int64_t tiles,
+                                                          double* __restrict__ partials) {
+  const int64_t row = (int64_t)blockIdx.y * P;
+  const GT* __restrict__ g = reinterpret_cast<const GT*>(gp) + row;
+  double acc = 0.0;
+  for (int64_t tile = blockIdx.x; tile < tiles; tile += gridDim.x) {
+    const int64_t base = tile * (int64_t)(kBlock * V * U);
+    float a[U][V];
+#pragma unroll
+    for (int k = 0; k < U; ++k) {
+      const int64_t e = base + ((int64_t)k * kBlock + threadIdx.x) * V;
+      if (e < P) load_v<GT, V, false>(g, e, a[k]);
+    }
+#pragma unroll
+    for (int k = 0; k < U; ++k) {
+      const int64_t e = base + ((int64_t)k * kBlock + threadIdx.x) * V;
+      if (e >= P) continue;
+#pragma unroll
+      for (int t = 0; t < V; ++t) {
+        const double d = (double)a[k][t];
+        acc = __builtin_fma(d, d, acc);
+      }
+    }
+  }
+  acc = wave_sum(acc);
+  __shared__ double ws[kBlock / 64];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  if (lane == 0) ws[wave] = acc;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    double t = 0.0;
+#pragma unroll
+    for (int i = 0; i < kBlock / 64; ++i) t += ws[i];
+    partials[(int64_t)blockIdx.y * gridDim.x + blockIdx.x] = t;
+  }
+}
+
+// scale[m] = min(1, rho / ||g^m||), 1 for a zero norm; one wavefront per replica.
+__global__ __launch_bounds__(64) void k_clip_finalize(const double* __restrict__ partials, int32_t nb,
+                                                      double rho, float* __restrict__ scale) {
+  const int32_t m = blockIdx.x;
+  double acc = 0.0;
+  for (int32_t i = threadIdx.x; i < nb; i += 64) acc += partials[(int64_t)m * nb + i];
+  acc = wave_sum(acc);
+  if (threadIdx.x == 0) {
+    const double norm = __builtin_sqrt(acc);
+    double c = 1.0;
+    if (norm > 0.0) {
+      c = rho / norm;
+      if (!(c < 1.0)) c = 1.0;
+    }
+    scale[m] = (float)c;
+  }
+}
+
+// ------------------------------------------------------------ init
+
+// Rows 1..K-1 of x <- row 0 (every worker starts from the same x_0).
+template <typename T>
+__global__ __launch_bounds__(kBlock) void k_broadcast_row0(T* __restrict__ x, int64_t P, int32_t K) {
+  const int64_t stride = (int64_t)gridDim.x * kBlock;
+  for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < P; i += stride) {
+    const T a = x[i];
+    for (int32_t m = 1; m < K; ++m) x[(int64_t)m * P + i] = a;
+  }
+}
+
+__global__ __launch_bounds__(kBlock) void k_fill_zero(float* __restrict__ a, int64_t n) {
+  const int64_t stride = (int64_t)gridDim.x * kBlock;
+  for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < n; i += stride) a[i] = 0.0f;
+}
+
+}  // namespace mtdao

@@ -1,0 +1,497 @@
+// Host side of the MT-DAO C ABI (include/mtdao.h): validation, the sync
+// schedule, per-step scalars, launch configuration and error mapping.
+// The arithmetic of every step runs in the kernels of kernels.hpp.
+
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "../../include/mtdao.h"
+#include "kernels.hpp"
+
+using namespace mtdao;
+
+struct mtdao_handle {
+  mtdao_config cfg;                 // copy; tensor_numel points into `tensors`
+  std::vector<int64_t> tensors;
+  void* x = nullptr;
+  float* u[MTDAO_MAX_N] = {nullptr, nullptr, nullptr, nullptr};
+  float* v = nullptr;
+  float* scale = nullptr;           // workspace: [K] clip factors
+  double* partials = nullptr;       // workspace: [K][norm_blocks]
+  int32_t norm_blocks = 0;
+  int64_t s = 0;                    // local updates applied
+  std::string err;
+};
+
+namespace {
+
+thread_local std::string g_err;
+
+constexpr int kStepU = 2;      // vector slots per thread in the local step
+constexpr int kNormU = 4;      // vector slots per thread in the norm pass
+constexpr int kNormBlocksMax = 512;
+
+int32_t fail(std::string* sink, int32_t code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  *sink = buf;
+  return code;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+int64_t esize(int32_t dt) { return dt == MTDAO_BF16 ? 2 : 4; }
+bool has_v(const mtdao_config& c) { return c.form != MTDAO_SGDM; }
+
+// Vector width of a row: 16-byte slots when every row start stays aligned.
+int vec_width(int32_t dtype_small, int64_t P) {
+  const int v = dtype_small == MTDAO_BF16 ? 8 : 4;
+  return (P % v == 0) ? v : 1;
+}
+
+int32_t validate(const mtdao_config* c, std::string* e) {
+  if (!c) return fail(e, MTDAO_ERR_INVALID_ARG, "config is NULL");
+  if (c->form < MTDAO_ADAM || c->form > MTDAO_SGDM)
+    return fail(e, MTDAO_ERR_INVALID_ARG, "form %d is not ADAM(0), ADOPT(1) or SGDM(2)", c->form);
+  if (c->replicas < 1 || c->replicas > MTDAO_MAX_REPLICAS)
+    return fail(e, MTDAO_ERR_INVALID_ARG, "replicas %d outside [1, %d]", c->replicas, MTDAO_MAX_REPLICAS);
+  if (c->n_moments < 1 || c->n_moments > MTDAO_MAX_N)
+    return fail(e, MTDAO_ERR_INVALID_ARG, "n_moments %d outside [1, %d]", c->n_moments, MTDAO_MAX_N);
+  if ((c->param_dtype != MTDAO_F32 && c->param_dtype != MTDAO_BF16) ||
+      (c->grad_dtype != MTDAO_F32 && c->grad_dtype != MTDAO_BF16))
+    return fail(e, MTDAO_ERR_INVALID_ARG, "param_dtype/grad_dtype must be F32(0) or BF16(1)");
+  if (c->adopt_order != MTDAO_ADOPT_PREV && c->adopt_order != MTDAO_ADOPT_CUR)
+    return fail(e, MTDAO_ERR_INVALID_ARG, "adopt_order %d is not PREV(0) or CUR(1)", c->adopt_order);
+  if (c->bias_correction != 0 && c->bias_correction != 1)
+    return fail(e, MTDAO_ERR_INVALID_ARG, "bias_correction must be 0 or 1");
+  double wsum = 0.0;
+  for (int j = 0; j < c->n_moments; ++j) {
+    const float b = c->beta1[j], w = c->omega[j];
+    if (!(b >= 0.0f && b < 1.0f)) return fail(e, MTDAO_ERR_INVALID_ARG, "beta1[%d]=%g outside [0,1)", j, b);
+    if (!(w >= 0.0f && w <= 1.0f)) return fail(e, MTDAO_ERR_INVALID_ARG, "omega[%d]=%g outside [0,1]", j, w);
+    if (c->period_u[j] < 0) return fail(e, MTDAO_ERR_INVALID_ARG, "period_u[%d]=%d < 0", j, c->period_u[j]);
+    wsum += (double)w;
+  }
+  if (wsum > 1.0 + 1e-6) return fail(e, MTDAO_ERR_INVALID_ARG, "sum of omega = %.9g exceeds 1", wsum);
+  if (has_v(*c)) {
+    if (!(c->beta2 >= 0.0f && c->beta2 < 1.0f))
+      return fail(e, MTDAO_ERR_INVALID_ARG, "beta2=%g outside [0,1)", c->beta2);
+    if (!(c->eps >= 0.0f) || !std::isfinite(c->eps))
+      return fail(e, MTDAO_ERR_INVALID_ARG, "eps=%g must be finite and >= 0", c->eps);
+    if (c->period_v < 0) return fail(e, MTDAO_ERR_INVALID_ARG, "period_v=%d < 0", c->period_v);
+  }
+  if (!std::isfinite(c->clip_rho)) return fail(e, MTDAO_ERR_INVALID_ARG, "clip_rho is not finite");
+  if (c->form == MTDAO_ADOPT && c->clip_rho > 0.0f)
+    return fail(e, MTDAO_ERR_INVALID_ARG, "ADOPT clips the normalised gradient with c_t (per call), not rho");
+  if (c->period_x < 0) return fail(e, MTDAO_ERR_INVALID_ARG, "period_x=%d < 0", c->period_x);
+  if (c->start_step < 0) return fail(e, MTDAO_ERR_INVALID_ARG, "start_step < 0");
+  if (c->numel < 0) return fail(e, MTDAO_ERR_INVALID_ARG, "numel < 0");
+  if (c->numel > (INT64_C(1) << 40) / c->replicas)
+    return fail(e, MTDAO_ERR_INVALID_ARG, "replicas * numel exceeds 2^40 elements");
+  if (c->n_tensors < 0) return fail(e, MTDAO_ERR_INVALID_ARG, "n_tensors < 0");
+  if (c->n_tensors > 0) {
+    if (!c->tensor_numel) return fail(e, MTDAO_ERR_INVALID_ARG, "tensor_numel is NULL");
+    int64_t sum = 0;
+    for (int32_t t = 0; t < c->n_tensors; ++t) {
+      if (c->tensor_numel[t] < 0) return fail(e, MTDAO_ERR_INVALID_ARG, "tensor_numel[%d] < 0", t);
+      sum += c->tensor_numel[t];
+      if (sum > c->numel) break;
+    }
+    if (sum != c->numel)
+      return fail(e, MTDAO_ERR_INVALID_ARG, "tensor_numel does not sum to numel=%lld", (long long)c->numel);
+  }
+  return MTDAO_OK;
+}
+
+uint32_t schedule_mask(const mtdao_config& c, int64_t s) {
+  uint32_t mask = 0;
+  if (c.period_x > 0 && s % c.period_x == 0) mask |= 1u;
+  for (int j = 0; j < c.n_moments; ++j)
+    if (c.period_u[j] > 0 && s % c.period_u[j] == 0) mask |= 1u << (j + 1);
+  if (has_v(c) && c.period_v > 0 && s % c.period_v == 0) mask |= 1u << (c.n_moments + 1);
+  return mask;
+}
+
+uint32_t valid_bits(const mtdao_config& c) {
+  const int nb = 1 + c.n_moments + (has_v(c) ? 1 : 0);
+  return (nb >= 32) ? 0xFFFFFFFFu : ((1u << nb) - 1u);
+}
+
+int32_t norm_blocks_for(int64_t P, int V) {
+  const int64_t per_block = (int64_t)kBlock * V * kNormU;
+  int64_t nb = (P + per_block - 1) / per_block;
+  if (nb < 1) nb = 1;
+  if (nb > kNormBlocksMax) nb = kNormBlocksMax;
+  return (int32_t)nb;
+}
+
+size_t workspace_for(const mtdao_config& c) {
+  if (!(c.clip_rho > 0.0f) || c.form == MTDAO_ADOPT) return 0;
+  const size_t scale_bytes = ((size_t)c.replicas * sizeof(float) + 255) / 256 * 256;
+  return scale_bytes + (size_t)c.replicas * kNormBlocksMax * sizeof(double);
+}
+
+// Non-overlap of two [lo, lo + bytes) device ranges.
+bool overlap(const void* a, int64_t abytes, const void* b, int64_t bbytes) {
+  const uintptr_t a0 = (uintptr_t)a, b0 = (uintptr_t)b;
+  return a0 < b0 + (uintptr_t)bbytes && b0 < a0 + (uintptr_t)abytes;
+}
+
+int32_t hip_check(std::string* e, hipError_t r, const char* what) {
+  if (r != hipSuccess) return fail(e, MTDAO_ERR_HIP, "%s: %s", what, hipGetErrorString(r));
+  return MTDAO_OK;
+}
+
+dim3 grid_for(int64_t tiles, int32_t ny) {
+  const int64_t maxx = INT64_C(0x7fffffff);
+  return dim3((unsigned)(tiles < maxx ? (tiles > 0 ? tiles : 1) : maxx), (unsigned)ny, 1);
+}
+
+// ---------------------------------------------------------------- dispatch
+
+template <int FORM, int N, typename XT, typename GT, int V>
+void launch_step_t(const StepParams& p, int32_t K, int order, hipStream_t st) {
+  dim3 grid = grid_for(p.tiles, K);
+  if constexpr (FORM == kAdopt) {
+    if (order == kCur) {
+      hipLaunchKernelGGL((k_local_step<FORM, N, XT, GT, V, kStepU, false, kCur>), grid, dim3(kBlock), 0, st, p);
+      return;
+    }
+  }
+  hipLaunchKernelGGL((k_local_step<FORM, N, XT, GT, V, kStepU, false, kPrev>), grid, dim3(kBlock), 0, st, p);
+}
+
+template <int FORM, int N, typename XT, typename GT>
+void launch_step_v(StepParams p, int32_t K, int V, int order, hipStream_t st) {
+  const int64_t per = (int64_t)kBlock * kStepU;
+  if (V == 1) {
+    p.tiles = (p.P + per - 1) / per;
+    launch_step_t<FORM, N, XT, GT, 1>(p, K, order, st);
+  } else if (V == 4) {
+    p.tiles = (p.P + per * 4 - 1) / (per * 4);
+    launch_step_t<FORM, N, XT, GT, 4>(p, K, order, st);
+  } else {
+    p.tiles = (p.P + per * 8 - 1) / (per * 8);
+    launch_step_t<FORM, N, XT, GT, 8>(p, K, order, st);
+  }
+}
+
+template <int FORM, int N>
+void launch_step_n(const StepParams& p, const mtdao_config& c, int V, hipStream_t st) {
+  const int K = c.replicas, o = c.adopt_order;
+  if (c.param_dtype == MTDAO_F32 && c.grad_dtype == MTDAO_F32) launch_step_v<FORM, N, float, float>(p, K, V, o, st);
+  else if (c.param_dtype == MTDAO_F32) launch_step_v<FORM, N, float, uint16_t>(p, K, V, o, st);
+  else if (c.grad_dtype == MTDAO_F32) launch_step_v<FORM, N, uint16_t, float>(p, K, V, o, st);
+  else launch_step_v<FORM, N, uint16_t, uint16_t>(p, K, V, o, st);
+}
+
+template <int FORM>
+void launch_step_f(const StepParams& p, const mtdao_config& c, int V, hipStream_t st) {
+  switch (c.n_moments) {
+    case 1: launch_step_n<FORM, 1>(p, c, V, st); break;
+    case 2: launch_step_n<FORM, 2>(p, c, V, st); break;
+    case 3: launch_step_n<FORM, 3>(p, c, V, st); break;
+    default: launch_step_n<FORM, 4>(p, c, V, st); break;
+  }
+}
+
+template <typename GT>
+void launch_adopt_init(const void* g, float* v, int64_t P, int32_t K, int V, hipStream_t st) {
+  const int64_t per = (int64_t)kBlock * kStepU;
+  if (V == 1) {
+    hipLaunchKernelGGL((k_adopt_init_v<GT, 1, kStepU, false>), grid_for((P + per - 1) / per, K), dim3(kBlock), 0, st,
+                       g, v, P, (P + per - 1) / per);
+  } else {
+    hipLaunchKernelGGL((k_adopt_init_v<GT, 4, kStepU, false>), grid_for((P + 4 * per - 1) / (4 * per), K), dim3(kBlock),
+                       0, st, g, v, P, (P + 4 * per - 1) / (4 * per));
+  }
+}
+
+template <typename GT>
+void launch_norm(const void* g, int64_t P, int32_t K, int V, int32_t nb, double* partials, hipStream_t st) {
+  const int64_t per = (int64_t)kBlock * kNormU;
+  if (V == 1) {
+    hipLaunchKernelGGL((k_sumsq_partial<GT, 1, kNormU>), dim3(nb, K), dim3(kBlock), 0, st, g, P, (P + per - 1) / per,
+                       partials);
+  } else {
+    hipLaunchKernelGGL((k_sumsq_partial<GT, 4, kNormU>), dim3(nb, K), dim3(kBlock), 0, st, g, P,
+                       (P + 4 * per - 1) / (4 * per), partials);
+  }
+}
+
+template <typename T>
+void launch_mean(MeanParams p, int nstates, int V, hipStream_t st) {
+  if (V == 1) {
+    p.tiles = (p.P + kBlock - 1) / kBlock;
+    hipLaunchKernelGGL((k_replica_mean<T, 1, false>), grid_for(p.tiles, nstates), dim3(kBlock), 0, st, p);
+  } else if (V == 4) {
+    p.tiles = (p.P + 4 * kBlock - 1) / (4 * kBlock);
+    hipLaunchKernelGGL((k_replica_mean<T, 4, false>), grid_for(p.tiles, nstates), dim3(kBlock), 0, st, p);
+  } else {
+    p.tiles = (p.P + 8 * kBlock - 1) / (8 * kBlock);
+    hipLaunchKernelGGL((k_replica_mean<T, 8, false>), grid_for(p.tiles, nstates), dim3(kBlock), 0, st, p);
+  }
+}
+
+int launch_blocks(int64_t n) {
+  int64_t b = (n + kBlock - 1) / kBlock;
+  if (b < 1) b = 1;
+  if (b > 65536) b = 65536;
+  return (int)b;
+}
+
+}  // namespace
+
+// ===================================================================== ABI
+
+extern "C" {
+
+int32_t mtdao_workspace_bytes(const mtdao_config* cfg, size_t* bytes) {
+  const int32_t r = validate(cfg, &g_err);
+  if (r != MTDAO_OK) return r;
+  if (!bytes) return fail(&g_err, MTDAO_ERR_INVALID_ARG, "bytes is NULL");
+  *bytes = workspace_for(*cfg);
+  return MTDAO_OK;
+}
+
+int32_t mtdao_schedule(const mtdao_config* cfg, int64_t s, uint32_t* mask) {
+  const int32_t r = validate(cfg, &g_err);
+  if (r != MTDAO_OK) return r;
+  if (!mask) return fail(&g_err, MTDAO_ERR_INVALID_ARG, "mask is NULL");
+  if (s < 1) return fail(&g_err, MTDAO_ERR_RANGE, "step %lld < 1", (long long)s);
+  *mask = schedule_mask(*cfg, s);
+  return MTDAO_OK;
+}
+
+int32_t mtdao_init(const mtdao_config* cfg, const mtdao_buffers* bufs, void* workspace, size_t workspace_bytes,
+                   void* hip_stream, mtdao_handle** out) {
+  int32_t r = validate(cfg, &g_err);
+  if (r != MTDAO_OK) return r;
+  if (!bufs || !out) return fail(&g_err, MTDAO_ERR_INVALID_ARG, "bufs or out is NULL");
+  const mtdao_config& c = *cfg;
+  const int64_t KP = (int64_t)c.replicas * c.numel;
+  const int N = c.n_moments;
+  // device pointers and their extents
+  std::vector<std::pair<const void*, int64_t>> ranges;
+  if (c.numel > 0) {
+    if (!bufs->x) return fail(&g_err, MTDAO_ERR_INVALID_ARG, "x is NULL");
+    ranges.push_back({bufs->x, KP * esize(c.param_dtype)});
+    for (int j = 0; j < N; ++j) {
+      if (!bufs->u[j]) return fail(&g_err, MTDAO_ERR_INVALID_ARG, "u[%d] is NULL", j);
+      ranges.push_back({bufs->u[j], KP * 4});
+    }
+    if (has_v(c)) {
+      if (!bufs->v) return fail(&g_err, MTDAO_ERR_INVALID_ARG, "v is NULL (Adam and ADOPT need it)");
+      ranges.push_back({bufs->v, KP * 4});
+    }
+    for (auto& rg : ranges)
+      if (!aligned16(rg.first)) return fail(&g_err, MTDAO_ERR_ALIGN, "a state buffer is not 16-byte aligned");
+    for (size_t a = 0; a < ranges.size(); ++a)
+      for (size_t b = a + 1; b < ranges.size(); ++b)
+        if (overlap(ranges[a].first, ranges[a].second, ranges[b].first, ranges[b].second))
+          return fail(&g_err, MTDAO_ERR_INVALID_ARG, "state buffers overlap");
+  }
+  const size_t need = workspace_for(c);
+  if (need > 0) {
+    if (!workspace) return fail(&g_err, MTDAO_ERR_WORKSPACE, "workspace of %zu bytes required", need);
+    if (workspace_bytes < need)
+      return fail(&g_err, MTDAO_ERR_WORKSPACE, "workspace %zu bytes < required %zu", workspace_bytes, need);
+    if ((reinterpret_cast<uintptr_t>(workspace) & 255u) != 0)
+      return fail(&g_err, MTDAO_ERR_ALIGN, "workspace is not 256-byte aligned");
+  }
+
+  mtdao_handle* h = new mtdao_handle();
+  h->cfg = c;
+  if (c.n_tensors > 0) h->tensors.assign(c.tensor_numel, c.tensor_numel + c.n_tensors);
+  else h->tensors.assign(1, c.numel);
+  h->cfg.n_tensors = (int32_t)h->tensors.size();
+  h->cfg.tensor_numel = h->tensors.data();
+  h->x = bufs->x;
+  for (int j = 0; j < N; ++j) h->u[j] = bufs->u[j];
+  h->v = has_v(c) ? bufs->v : nullptr;
+  h->s = c.start_step;
+  if (need > 0) {
+    const size_t scale_bytes = ((size_t)c.replicas * sizeof(float) + 255) / 256 * 256;
+    h->scale = reinterpret_cast<float*>(workspace);
+    h->partials = reinterpret_cast<double*>(reinterpret_cast<char*>(workspace) + scale_bytes);
+    h->norm_blocks = norm_blocks_for(c.numel, (c.numel % 4 == 0) ? 4 : 1);
+  }
+
+  hipStream_t st = reinterpret_cast<hipStream_t>(hip_stream);
+  if (!bufs->init_states && c.numel > 0) {
+    const int nb = launch_blocks(c.numel);
+    if (c.replicas > 1) {
+      if (c.param_dtype == MTDAO_F32)
+        hipLaunchKernelGGL(k_broadcast_row0<float>, dim3(nb), dim3(kBlock), 0, st, (float*)h->x, c.numel, c.replicas);
+      else
+        hipLaunchKernelGGL(k_broadcast_row0<uint16_t>, dim3(nb), dim3(kBlock), 0, st, (uint16_t*)h->x, c.numel,
+                           c.replicas);
+    }
+    const int zb = launch_blocks(KP);
+    for (int j = 0; j < N; ++j) hipLaunchKernelGGL(k_fill_zero, dim3(zb), dim3(kBlock), 0, st, h->u[j], KP);
+    if (h->v) hipLaunchKernelGGL(k_fill_zero, dim3(zb), dim3(kBlock), 0, st, h->v, KP);
+    r = hip_check(&g_err, hipGetLastError(), "mtdao_init launch");
+    if (r != MTDAO_OK) {
+      delete h;
+      return r;
+    }
+  }
+  g_err.clear();
+  *out = h;
+  return MTDAO_OK;
+}
+
+int32_t mtdao_local_step(mtdao_handle* h, const void* grads, float lr, float adopt_clip, void* hip_stream) {
+  if (!h) return fail(&g_err, MTDAO_ERR_INVALID_ARG, "handle is NULL");
+  const mtdao_config& c = h->cfg;
+  const int64_t P = c.numel, KP = (int64_t)c.replicas * P;
+  if (!std::isfinite(lr)) return fail(&h->err, MTDAO_ERR_INVALID_ARG, "lr is not finite");
+  if (!std::isfinite(adopt_clip)) return fail(&h->err, MTDAO_ERR_INVALID_ARG, "adopt_clip is not finite");
+  if (P > 0) {
+    if (!grads) return fail(&h->err, MTDAO_ERR_INVALID_ARG, "grads is NULL");
+    if (!aligned16(grads)) return fail(&h->err, MTDAO_ERR_ALIGN, "grads is not 16-byte aligned");
+    const int64_t gb = KP * esize(c.grad_dtype);
+    bool ov = overlap(grads, gb, h->x, KP * esize(c.param_dtype));
+    for (int j = 0; j < c.n_moments; ++j) ov = ov || overlap(grads, gb, h->u[j], KP * 4);
+    if (h->v) ov = ov || overlap(grads, gb, h->v, KP * 4);
+    if (ov) return fail(&h->err, MTDAO_ERR_INVALID_ARG, "grads overlaps a state buffer");
+  }
+  const int64_t s = h->s + 1;
+  h->s = s;
+  if (P == 0) return MTDAO_OK;
+  hipStream_t st = reinterpret_cast<hipStream_t>(hip_stream);
+
+  // per-step scalars in double, rounded once to fp32
+  StepParams p;
+  std::memset(&p, 0, sizeof p);
+  p.x = h->x;
+  p.g = grads;
+  for (int j = 0; j < c.n_moments; ++j) p.u[j] = h->u[j];
+  p.v = h->v;
+  p.P = P;
+  double wsum = 0.0;
+  const bool bc = c.form == MTDAO_ADAM && c.bias_correction;
+  for (int j = 0; j < c.n_moments; ++j) {
+    const double b = c.beta1[j], w = c.omega[j];
+    p.beta[j] = c.beta1[j];
+    p.omb[j] = (float)(1.0 - b);
+    p.w[j] = (float)(bc ? w / (1.0 - std::pow(b, (double)s)) : w);
+    wsum += w;
+  }
+  p.gw = (float)(1.0 - wsum);
+  p.beta2 = c.beta2;
+  p.omb2 = (float)(1.0 - (double)c.beta2);
+  p.inv_bc2 = (float)(bc ? 1.0 / (1.0 - std::pow((double)c.beta2, (double)s)) : 1.0);
+  p.eps = c.eps;
+  p.lr = lr;
+  p.clip = adopt_clip;
+  p.scale = nullptr;
+
+  const int Vg = (P % 4 == 0) ? 4 : 1;  // 16-byte (fp32) or 8-byte (bf16) slots
+  if (c.form != MTDAO_ADOPT && c.clip_rho > 0.0f) {
+    if (c.grad_dtype == MTDAO_F32) launch_norm<float>(grads, P, c.replicas, Vg, h->norm_blocks, h->partials, st);
+    else launch_norm<uint16_t>(grads, P, c.replicas, Vg, h->norm_blocks, h->partials, st);
+    hipLaunchKernelGGL(k_clip_finalize, dim3(c.replicas), dim3(64), 0, st, h->partials, h->norm_blocks,
+                       (double)c.clip_rho, h->scale);
+    p.scale = h->scale;
+  }
+  // one vector width for every buffer the step touches
+  const int V = (c.param_dtype == MTDAO_BF16 || c.grad_dtype == MTDAO_BF16) ? vec_width(MTDAO_BF16, P)
+                                                                              : vec_width(MTDAO_F32, P);
+  if (c.form == MTDAO_ADOPT && c.adopt_order == MTDAO_ADOPT_PREV && s == 1) {
+    const int Vi = (P % 4 == 0) ? 4 : 1;
+    if (c.grad_dtype == MTDAO_F32) launch_adopt_init<float>(grads, h->v, P, c.replicas, Vi, st);
+    else launch_adopt_init<uint16_t>(grads, h->v, P, c.replicas, Vi, st);
+  } else if (c.form == MTDAO_ADAM) {
+    launch_step_f<kAdam>(p, c, V, st);
+  } else if (c.form == MTDAO_ADOPT) {
+    launch_step_f<kAdopt>(p, c, V, st);
+  } else {
+    launch_step_f<kSgdm>(p, c, V, st);
+  }
+  return hip_check(&h->err, hipGetLastError(), "mtdao_local_step launch");
+}
+
+int32_t mtdao_sync(mtdao_handle* h, uint32_t mask, uint32_t* applied_mask, void* hip_stream) {
+  if (!h) return fail(&g_err, MTDAO_ERR_INVALID_ARG, "handle is NULL");
+  const mtdao_config& c = h->cfg;
+  uint32_t m;
+  if (mask == MTDAO_SYNC_AUTO) {
+    m = h->s >= 1 ? schedule_mask(c, h->s) : 0u;
+  } else {
+    if (mask & ~valid_bits(c))
+      return fail(&h->err, MTDAO_ERR_INVALID_ARG, "mask 0x%x has bits beyond the %d states", mask,
+                  1 + c.n_moments + (has_v(c) ? 1 : 0));
+    m = mask;
+  }
+  if (applied_mask) *applied_mask = m;
+  if (m == 0 || c.numel == 0 || c.replicas == 1) return MTDAO_OK;  // K = 1: the mean is the row
+  hipStream_t st = reinterpret_cast<hipStream_t>(hip_stream);
+  MeanParams mp;
+  std::memset(&mp, 0, sizeof mp);
+  mp.P = c.numel;
+  mp.K = c.replicas;
+  // fp32 moment states (and fp32 x) in one launch, bf16 x in its own
+  int n = 0;
+  if ((m & 1u) && c.param_dtype == MTDAO_F32) mp.state[n++] = h->x;
+  for (int j = 0; j < c.n_moments; ++j)
+    if (m & (1u << (j + 1))) mp.state[n++] = h->u[j];
+  if (h->v && (m & (1u << (c.n_moments + 1)))) mp.state[n++] = h->v;
+  if (n > 0) launch_mean<float>(mp, n, vec_width(MTDAO_F32, c.numel), st);
+  if ((m & 1u) && c.param_dtype == MTDAO_BF16) {
+    MeanParams xp = mp;
+    xp.state[0] = h->x;
+    launch_mean<uint16_t>(xp, 1, vec_width(MTDAO_BF16, c.numel), st);
+  }
+  return hip_check(&h->err, hipGetLastError(), "mtdao_sync launch");
+}
+
+int32_t mtdao_read_state(mtdao_handle* h, int32_t state, int32_t replica, int64_t offset, int64_t count,
+                         void* host_dst, void* hip_stream) {
+  if (!h) return fail(&g_err, MTDAO_ERR_INVALID_ARG, "handle is NULL");
+  const mtdao_config& c = h->cfg;
+  const int32_t nstates = 1 + c.n_moments + (has_v(c) ? 1 : 0);
+  if (state < 0 || state >= nstates)
+    return fail(&h->err, MTDAO_ERR_INVALID_ARG, "state %d outside [0, %d)", state, nstates);
+  if (replica < 0 || replica >= c.replicas)
+    return fail(&h->err, MTDAO_ERR_RANGE, "replica %d outside [0, %d)", replica, c.replicas);
+  if (offset < 0 || count < 0 || offset > c.numel || count > c.numel - offset)
+    return fail(&h->err, MTDAO_ERR_RANGE, "range [%lld, +%lld) outside [0, %lld)", (long long)offset,
+                (long long)count, (long long)c.numel);
+  if (count == 0) return MTDAO_OK;
+  if (!host_dst) return fail(&h->err, MTDAO_ERR_INVALID_ARG, "host_dst is NULL");
+  const void* base;
+  int64_t es;
+  if (state == 0) {
+    base = h->x;
+    es = esize(c.param_dtype);
+  } else if (state <= c.n_moments) {
+    base = h->u[state - 1];
+    es = 4;
+  } else {
+    base = h->v;
+    es = 4;
+  }
+  const char* src = reinterpret_cast<const char*>(base) + ((int64_t)replica * c.numel + offset) * es;
+  hipStream_t st = reinterpret_cast<hipStream_t>(hip_stream);
+  int32_t r = hip_check(&h->err, hipMemcpyAsync(host_dst, src, (size_t)(count * es), hipMemcpyDeviceToHost, st),
+                        "mtdao_read_state copy");
+  if (r != MTDAO_OK) return r;
+  return hip_check(&h->err, hipStreamSynchronize(st), "mtdao_read_state wait");
+}
+
+int64_t mtdao_step_count(const mtdao_handle* h) { return h ? h->s : -1; }
+
+const char* mtdao_last_error(const mtdao_handle* h) { return h ? h->err.c_str() : g_err.c_str(); }
+
+void mtdao_destroy(mtdao_handle* h) { delete h; }
+
+}  // extern "C"

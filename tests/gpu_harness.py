@@ -1,0 +1,197 @@
+"""Shared pieces of the GPU parity tests: run a workload through the C ABI on
+the GPU, run the CPU oracle on the same seeded inputs (all elements or a
+deterministic sample), and compare.
+
+Inputs for both sides come from ``synth``; no oracle input or expected
+value is ever taken from the GPU path.
+"""
+
+from __future__ import annotations
+
+import math
+import sys
+from dataclasses import dataclass
+from typing import Dict, List, Optional, Sequence
+
+import numpy as np
+import torch
+
+import oracle
+import synth
+from paper_2510_05361_amd import mtdao as abi
+from paper_2510_05361_amd.optimizer import MtdaoOptimizer
+from synth.device import DeviceInputs
+
+# Tolerances (derivations in the design notes):
+#  fp32 states: max_i |a_i - b_i| / max(|b_i|, rms(b)) <= 1e-5
+#  bf16 params: within 3 bf16 ulps everywhere, <= 1e-3 of the elements more
+#  than 1 ulp apart and <= 2e-2 of them 1 ulp apart (a rounding decision
+#  taken on an fp32 value a few fp32 ulps from the fp64 one flips now and
+#  then; the flip persists because x feeds the next update).
+REL_TOL = 1e-5
+BF16_MAX_ULPS = 3
+BF16_FRAC_GT1 = 1e-3
+BF16_FRAC_GE1 = 2e-2
+
+
+def log(msg: str) -> None:
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def device() -> torch.device:
+    return torch.device("cuda:0")
+
+
+# ------------------------------------------------------------------ oracle
+
+
+def oracle_cfg(w: synth.Workload) -> oracle.OracleConfig:
+    return oracle.OracleConfig.from_workload(w)
+
+
+_SUMSQ_CACHE: Dict[tuple, float] = {}
+
+
+def oracle_clip_scales(w: synth.Workload, s: int) -> Optional[np.ndarray]:
+    """Per-worker clip factors from the oracle over the FULL gradient of
+    step s.  Large rows use their periodic structure: a row is the scaled
+    pool rotated by the worker's offset and repeated, so its sum of squares
+    is q * sumsq(whole scaled pool) + sumsq(first r rotated values)."""
+    if not w.clip_rho > 0 or w.form == "adopt":
+        return None
+    P = w.numel
+    if P <= 1 << 22:
+        return oracle.clip_scales(oracle_cfg(w), synth.host_grad_rows(w, s))
+    sig = w.tensor_sigmas()
+    assert np.all(sig == sig[0]) and w.grad_dtype == "f32"
+    scaled = (sig[0] * synth.grad_pool(w)).astype(np.float32)
+    key = (w.grad_dist, w.seed_g, float(sig[0]))
+    if key not in _SUMSQ_CACHE:
+        _SUMSQ_CACHE[key] = oracle.sumsq(scaled)
+    q, r = divmod(P, synth.POOL_SIZE)
+    out = np.empty(w.replicas)
+    for m in range(w.replicas):
+        off = synth.grad_offset(w.seed_g, m, s)
+        head = scaled[off:off + r]
+        tail = scaled[:max(0, r - head.size)]
+        total = q * _SUMSQ_CACHE[key] + oracle.sumsq(head) + oracle.sumsq(tail)
+        out[m] = oracle.clip_scale(math.sqrt(total), w.clip_rho)
+    return out
+
+
+@dataclass
+class OracleResult:
+    state: oracle.OracleState
+    masks: List[int]
+    idx: Optional[np.ndarray]
+
+
+def run_oracle(w: synth.Workload, steps: Sequence[int], idx: Optional[np.ndarray] = None,
+               init: Optional[oracle.OracleState] = None) -> OracleResult:
+    """Oracle over elements ``idx`` (all if None) for global steps ``steps``.
+    Each element's trajectory depends only on its own inputs and, through
+    the clip, on the per-worker norms, which are taken over full rows."""
+    cfg = oracle_cfg(w)
+    if init is None:
+        st = oracle.new_state(cfg, synth.host_x0_row(w, idx), w.replicas)
+    else:
+        st = init
+    masks = oracle.run(cfg, st, lambda s: synth.host_grad_rows(w, s, idx), steps, lambda s: w.lr,
+                       w.adopt_clip_value, scales=lambda s, g: oracle_clip_scales(w, s))
+    return OracleResult(st, masks, idx)
+
+
+# ------------------------------------------------------------------ GPU
+
+
+@dataclass
+class GpuResult:
+    opt: MtdaoOptimizer
+    masks: List[int]
+
+
+def run_gpu(w: synth.Workload, steps: Sequence[int], start_step: int = 0, dev: Optional[DeviceInputs] = None,
+            opt: Optional[MtdaoOptimizer] = None, grads: Optional[torch.Tensor] = None) -> GpuResult:
+    d = device()
+    dev = dev or DeviceInputs(w, d)
+    if opt is None:
+        cfg = abi.config_from_workload(w, start_step=start_step)
+        opt = MtdaoOptimizer(cfg, d, x0=dev.x0_row())
+    gdt = torch.bfloat16 if w.grad_dtype == "bf16" else torch.float32
+    if grads is None:
+        grads = torch.empty((w.replicas, w.numel), dtype=gdt, device=d)
+    masks = []
+    for s in steps:
+        dev.grads_into(s, grads)
+        opt.step(grads, w.lr, w.adopt_clip_value(s))
+        masks.append(opt.sync())
+    torch.cuda.synchronize()
+    return GpuResult(opt, masks)
+
+
+def gather_state(t: torch.Tensor, idx: Optional[np.ndarray]) -> np.ndarray:
+    """Host copy of a [K][P] device state (all columns, or columns idx);
+    bf16 states come back as uint16 bit patterns."""
+    if idx is not None:
+        t = t[:, torch.from_numpy(idx).to(t.device)]
+    if t.dtype == torch.bfloat16:
+        return t.contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+    return t.cpu().numpy()
+
+
+# ------------------------------------------------------------------ compare
+
+
+def rel_err(a: np.ndarray, b: np.ndarray) -> float:
+    a = np.asarray(a, dtype=np.float64)
+    b = np.asarray(b, dtype=np.float64)
+    rms = math.sqrt(float(np.mean(b * b))) if b.size else 0.0
+    den = np.maximum(np.abs(b), rms)
+    err = np.abs(a - b)
+    if not np.all(np.isfinite(a)):
+        return float("inf")
+    with np.errstate(invalid="ignore", divide="ignore"):
+        r = np.where(den > 0, err / np.where(den > 0, den, 1.0), err)
+    return float(r.max()) if r.size else 0.0
+
+
+def bf16_ulps(a_bits: np.ndarray, b_bits: np.ndarray) -> np.ndarray:
+    def ordered(bits):
+        i = bits.astype(np.int32)
+        return np.where(i & 0x8000, -(i & 0x7FFF), i)
+    return np.abs(ordered(a_bits) - ordered(b_bits))
+
+
+def compare(w: synth.Workload, gpu: MtdaoOptimizer, orc: OracleResult, label: str) -> Dict[str, float]:
+    """Every state of every replica against the oracle; raises on failure."""
+    names = ["x"] + [f"u{j + 1}" for j in range(w.n_moments)] + (["v"] if w.has_v else [])
+    gs = gpu.states()
+    os_ = orc.state.arrays()
+    report = {}
+    for name, g, o in zip(names, gs, os_):
+        a = gather_state(g, orc.idx)
+        if name == "x" and w.param_dtype == "bf16":
+            ul = bf16_ulps(a, o)
+            n = ul.size
+            stats = dict(max_ulps=int(ul.max()), frac_ge1=float((ul >= 1).sum() / n),
+                         frac_gt1=float((ul > 1).sum() / n))
+            report[name] = stats
+            log(f"  {label} {name}: {stats}")
+            assert stats["max_ulps"] <= BF16_MAX_ULPS, (label, name, stats)
+            assert stats["frac_gt1"] <= BF16_FRAC_GT1, (label, name, stats)
+            assert stats["frac_ge1"] <= BF16_FRAC_GE1, (label, name, stats)
+        else:
+            e = rel_err(a, o)
+            report[name] = e
+            log(f"  {label} {name}: rel_err={e:.3e}")
+            assert e <= REL_TOL, (label, name, e)
+    return report
+
+
+def free(*objs) -> None:
+    for o in objs:
+        if isinstance(o, GpuResult):
+            o.opt.close()
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()

@@ -1,0 +1,263 @@
+"""GPU path (C ABI, gfx950 kernels) against the CPU oracle.
+
+Small variants of every workload run their full step sequence and are
+compared on every element; the full-size workloads run in the launch
+configuration the benchmark times and are compared on a deterministic
+element sample (each element's trajectory depends only on its own inputs
+and on the per-worker clip norms, which the oracle takes over full rows).
+The applied sync mask of every step must equal the oracle's bit for bit.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+from gpu_harness import compare, free, gather_state, log, run_gpu, run_oracle
+from paper_2510_05361_amd import mtdao as abi
+from paper_2510_05361_amd.optimizer import MtdaoOptimizer
+from synth.device import DeviceInputs
+
+pytestmark = pytest.mark.gpu
+
+NAMES = list(synth.WORKLOADS)
+
+
+def _steps(w, start=0):
+    return list(range(start + 1, w.steps + 1))
+
+
+@pytest.mark.parametrize("tail", [40, 37], ids=["aligned_tail", "odd_tail"])
+@pytest.mark.parametrize("name", NAMES)
+def test_small_variant_full_compare(name, tail):
+    """~60k elements per replica (tens of tiles) plus a ragged tail; the
+    odd tail takes the scalar path of every kernel."""
+    w = synth.small_variant(synth.WORKLOADS[name], 60_000, tail=tail)
+    log(f"case small {w.name} P={w.numel} K={w.replicas} T={w.steps}")
+    g = run_gpu(w, _steps(w))
+    o = run_oracle(w, _steps(w))
+    assert g.masks == o.masks
+    assert any(g.masks)
+    compare(w, g.opt, o, w.name)
+    free(g)
+
+
+@pytest.mark.parametrize("name", NAMES)
+def test_full_size_sampled(name):
+    w = synth.WORKLOADS[name]
+    idx = synth.sample_indices(w)
+    log(f"case full {w.name} P={w.numel} K={w.replicas} T={w.steps} sample={idx.size}")
+    g = run_gpu(w, _steps(w))
+    log("  gpu done")
+    o = run_oracle(w, _steps(w), idx)
+    assert g.masks == o.masks
+    compare(w, g.opt, o, w.name)
+    free(g)
+
+
+EDGE = {
+    "one_replica": dict(replicas=1),
+    "four_moments": dict(beta1=(0.0, 0.5, 0.9, 0.999), omega=(0.1, 0.2, 0.3, 0.4),
+                         period_u=(1, 3, 0, 5)),
+    "no_moment_weight": dict(omega=(0.0, 0.0)),
+    "all_moment_weight": dict(omega=(0.25, 0.75)),
+    "zero_betas": dict(beta1=(0.0, 0.0)),
+    "all_periods_one": dict(period_x=1, period_u=(1, 1), period_v=1),
+    "never_sync": dict(period_x=0, period_u=(0, 0), period_v=0),
+}
+
+
+@pytest.mark.parametrize("form", ["adam", "adopt", "sgdm"])
+@pytest.mark.parametrize("edge", list(EDGE))
+def test_edge_cases(form, edge):
+    base = {"adam": "adam_n2_k2_p1m", "adopt": "adopt_n2_k8_p124m_bf16",
+            "sgdm": "sgdm_n2_k16_p354m_clip"}[form]
+    w = synth.small_variant(synth.WORKLOADS[base], 9_000, tail=12)
+    kw = dict(steps=min(w.steps, 24), replicas=min(w.replicas, 4))
+    kw.update(EDGE[edge])
+    w = w.replace(**kw)
+    if edge == "four_moments" and form == "sgdm":
+        w = w.replace(omega=(0.1, 0.2, 0.3, 0.3))
+    log(f"case edge {edge} {form} P={w.numel} K={w.replicas}")
+    g = run_gpu(w, _steps(w))
+    o = run_oracle(w, _steps(w))
+    assert g.masks == o.masks
+    compare(w, g.opt, o, f"{edge}-{form}")
+    if edge == "all_periods_one":
+        for t in g.opt.states():
+            assert torch.equal(t, t[0:1].expand_as(t)), "replicas differ after an every-step sync"
+    free(g)
+
+
+@pytest.mark.parametrize("variant", ["adopt_cur", "f32_params_bf16_grads", "bf16_params_f32_grads",
+                                     "adam_with_clip", "start_step_offset"])
+def test_variants(variant):
+    if variant == "adopt_cur":
+        w = synth.small_variant(synth.WORKLOADS["adopt_n2_k8_p124m_bf16"], 30_000, tail=8).replace(
+            adopt_order="cur", steps=40)
+    elif variant == "f32_params_bf16_grads":
+        w = synth.small_variant(synth.WORKLOADS["adam_n3_k4_p16m"], 30_000, tail=8).replace(
+            grad_dtype="bf16", steps=40)
+    elif variant == "bf16_params_f32_grads":
+        w = synth.small_variant(synth.WORKLOADS["adopt_n2_k8_p124m_bf16"], 30_000, tail=16).replace(
+            grad_dtype="f32", steps=40)
+    elif variant == "adam_with_clip":
+        w = synth.small_variant(synth.WORKLOADS["adam_n3_k4_p16m"], 30_000, tail=4).replace(
+            clip_rho=0.05, steps=40)
+    else:
+        w = synth.small_variant(synth.WORKLOADS["adam_n2_k2_p1m"], 30_000).replace(steps=40)
+    log(f"case variant {variant}")
+    start = 1000 if variant == "start_step_offset" else 0
+    g = run_gpu(w, list(range(start + 1, start + w.steps + 1)), start_step=start)
+    o = run_oracle(w, list(range(start + 1, start + w.steps + 1)))
+    assert g.masks == o.masks
+    compare(w, g.opt, o, variant)
+    free(g)
+
+
+def test_zero_gradient_replica_and_zero_gradients():
+    """A worker whose gradient is all zero has norm 0 and clip factor 1."""
+    w = synth.small_variant(synth.WORKLOADS["sgdm_n2_k16_p354m_clip"], 20_000).replace(
+        replicas=3, steps=6)
+    d = torch.device("cuda:0")
+    dev = DeviceInputs(w, d)
+    cfg = abi.config_from_workload(w)
+    opt = MtdaoOptimizer(cfg, d, x0=dev.x0_row())
+    ocfg = oracle.OracleConfig.from_workload(w)
+    ost = oracle.new_state(ocfg, synth.host_x0_row(w), w.replicas)
+    grads = torch.empty((w.replicas, w.numel), dtype=torch.float32, device=d)
+    for s in range(1, w.steps + 1):
+        dev.grads_into(s, grads)
+        grads[1].zero_()
+        if s == 3:
+            grads.zero_()
+        hg = grads.cpu().numpy()  # built by torch from the seeded pool, not by the library
+        hg2 = synth.host_grad_rows(w, s)
+        hg2[1] = 0
+        if s == 3:
+            hg2[:] = 0
+        assert np.array_equal(hg, hg2)
+        opt.step(grads, w.lr)
+        m = opt.sync()
+        oracle.run(ocfg, ost, lambda s_: hg2, [s], lambda s_: w.lr)
+        assert m == oracle.schedule(ocfg, s)
+    torch.cuda.synchronize()
+    from gpu_harness import OracleResult
+    compare(w, opt, OracleResult(ost, [], None), "zero-grad")
+    opt.close()
+
+
+def test_resume_is_bit_identical():
+    """Checkpoint/resume: read every state with mtdao_read_state, destroy,
+    re-init with init_states=1 and start_step=s, continue: bit-identical to
+    an uninterrupted run (bias correction and schedule depend only on s)."""
+    w = synth.small_variant(synth.WORKLOADS["adam_n3_k4_p16m"], 40_000, tail=8).replace(steps=70)
+    d = torch.device("cuda:0")
+    dev = DeviceInputs(w, d)
+    full = run_gpu(w, _steps(w), dev=dev)
+    cut = 37
+    a = run_gpu(w.replace(steps=cut), list(range(1, cut + 1)), dev=dev)
+    K, P = w.replicas, w.numel
+    host = []
+    for sid, t in enumerate(a.opt.states()):
+        rows = np.empty((K, P), dtype=np.float32)
+        for m in range(K):
+            abi.mtdao_read_state(a.opt.handle, sid, m, 0, P, rows[m], torch.cuda.current_stream().cuda_stream)
+        assert np.array_equal(rows, t.cpu().numpy())
+        host.append(rows)
+    assert abi.mtdao_step_count(a.opt.handle) == cut
+    a.opt.close()
+    del a
+    torch.cuda.empty_cache()
+    tx = torch.from_numpy(host[0]).to(d)
+    tu = [torch.from_numpy(h).to(d) for h in host[1:1 + w.n_moments]]
+    tv = torch.from_numpy(host[-1]).to(d)
+    cfg = abi.config_from_workload(w, start_step=cut)
+    opt = MtdaoOptimizer(cfg, d, resume=True, x=tx, u=tu, v=tv)
+    b = run_gpu(w, list(range(cut + 1, w.steps + 1)), dev=dev, opt=opt)
+    assert full.masks[cut:] == b.masks
+    for p, q in zip(full.opt.states(), b.opt.states()):
+        assert torch.equal(p, q)
+    free(full, b)
+
+
+def test_sync_idempotent_and_explicit_masks():
+    w = synth.small_variant(synth.WORKLOADS["adopt_n2_k8_p124m_bf16"], 30_000, tail=8).replace(
+        steps=5, period_x=0, period_u=(0, 0), period_v=0)
+    g = run_gpu(w, _steps(w))
+    o = run_oracle(w, _steps(w))
+    ocfg = oracle.OracleConfig.from_workload(w)
+    for mask in [0b0010, 0b1001, 0b1111]:
+        assert g.opt.sync(mask) == mask
+        before = [t.clone() for t in g.opt.states()]
+        assert g.opt.sync(mask) == mask  # averaging identical rows is an exact no-op
+        torch.cuda.synchronize()
+        for p, q in zip(before, g.opt.states()):
+            assert torch.equal(p, q)
+        oracle.sync(ocfg, o.state, mask)
+        compare(w, g.opt, o, f"mask{mask:04b}")
+    free(g)
+
+
+def test_deterministic():
+    """Two runs of the clipped SGDM workload are bit-identical (fixed-order
+    norm reduction, no atomics)."""
+    w = synth.small_variant(synth.WORKLOADS["sgdm_n2_k16_p354m_clip"], 200_000).replace(steps=20)
+    a = run_gpu(w, _steps(w))
+    b = run_gpu(w, _steps(w))
+    for p, q in zip(a.opt.states(), b.opt.states()):
+        assert torch.equal(p, q)
+    free(a, b)
+
+
+def test_guard_bands_untouched():
+    """Canary regions around every buffer (states, gradients, workspace)
+    keep their contents through init, steps and syncs."""
+    w = synth.small_variant(synth.WORKLOADS["sgdm_n2_k16_p354m_clip"], 30_000, tail=37).replace(
+        replicas=5, steps=40, period_x=3, period_u=(2, 5))
+    d = torch.device("cuda:0")
+    K, P, pad = w.replicas, w.numel, 4096
+    canary = float.fromhex("0x1.5555p-3")
+
+    def guarded(dtype):
+        big = torch.full((K * P + 2 * pad,), canary, dtype=dtype, device=d)
+        return big, big[pad:pad + K * P].view(K, P)
+
+    bx, x = guarded(torch.float32)
+    bu = [guarded(torch.float32) for _ in range(2)]
+    bg, grads = guarded(torch.float32)
+    dev = DeviceInputs(w, d)
+    x[0].copy_(dev.x0_row())
+    cfg = abi.config_from_workload(w)
+    ws_bytes = abi.mtdao_workspace_bytes(cfg)
+    wsbig = torch.full((ws_bytes + 2 * 4096,), 0xA5, dtype=torch.uint8, device=d)
+    bufs = abi.make_buffers(x.data_ptr(), [t.data_ptr() for _, t in bu], None, False)
+    h = abi.mtdao_init(cfg, bufs, wsbig[4096:].data_ptr(), ws_bytes, torch.cuda.current_stream().cuda_stream)
+    for s in range(1, w.steps + 1):
+        dev.grads_into(s, grads)
+        abi.mtdao_local_step(h, grads.data_ptr(), w.lr, 0.0, torch.cuda.current_stream().cuda_stream)
+        abi.mtdao_sync(h, abi.MTDAO_SYNC_AUTO, torch.cuda.current_stream().cuda_stream)
+    torch.cuda.synchronize()
+    for big in [bx, bg] + [b for b, _ in bu]:
+        assert torch.all(big[:pad] == canary) and torch.all(big[pad + K * P:] == canary)
+    assert torch.all(wsbig[:4096] == 0xA5) and torch.all(wsbig[4096 + ws_bytes:] == 0xA5)
+    abi.mtdao_destroy(h)
+
+
+def test_row_longer_than_2_pow_31():
+    """One replica row of 2^31 + 1000 fp32 elements (64-bit indexing, ragged
+    end): SGDM N=1, sampled around the 2^31 boundary and the end."""
+    P = (1 << 31) + 1000
+    w = synth.Workload(name="sgdm_long_row", replicas=1, form="sgdm", beta1=(0.9,), omega=(0.5,),
+                       beta2=0.0, eps=0.0, lr=1e-2, clip_rho=0.0, adopt_order="prev", adopt_clip="off",
+                       period_x=0, period_u=(0,), period_v=0, steps=3, param_dtype="f32",
+                       grad_dtype="f32", tensors=(synth.TensorSpec("flat", P, "matrix"),),
+                       grad_dist="normal", grad_std=1e-2, seed_g=1009)
+    idx = np.unique(np.concatenate([np.arange(0, 64), np.arange((1 << 31) - 64, (1 << 31) + 64),
+                                    np.arange(P - 64, P), np.arange(0, P, P // 4096)])).astype(np.int64)
+    log(f"case long row P={P}")
+    g = run_gpu(w, _steps(w))
+    o = run_oracle(w, _steps(w), idx)
+    compare(w, g.opt, o, "long-row")
+    free(g)
