@@ -33,7 +33,8 @@ sys.path.insert(0, ROOT)
 METRIC = "param-element updates/s (x K workers) + achieved HBM GB/s % peak, step & sync"
 HBM_PEAK_GBS = 8000.0
 DEFAULT_WORKLOAD = "adam_n3_k4_p1311m"
-KERNEL_SRC = os.path.join(ROOT, "paper_2510_05361_amd", "csrc", "kernels.hpp")
+KERNEL_SRCS = [os.path.join(ROOT, "paper_2510_05361_amd", "csrc", f) for f in ("kernels.hpp", "mtdao.hip")]
+STREAM_LIB = os.path.join(ROOT, "paper_2510_05361_amd", "libstream_ref.so")
 
 
 def step_bytes_per_element(w) -> int:
@@ -53,8 +54,52 @@ def norm_bytes_per_element(w) -> int:
 
 
 def kernel_hash() -> str:
-    with open(KERNEL_SRC, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    """Hash of the kernel source and its launch configuration."""
+    h = hashlib.sha256()
+    for p in KERNEL_SRCS:
+        with open(p, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def stream_lib():
+    import ctypes
+
+    L = ctypes.CDLL(STREAM_LIB)
+    for n in ("stream_ref_copy", "stream_ref_read"):
+        getattr(L, n).argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p]
+        getattr(L, n).restype = ctypes.c_int32
+    L.stream_ref_fill.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p]
+    L.stream_ref_fill.restype = ctypes.c_int32
+    return L
+
+
+def achievable(nbytes: int = 8 << 30, reps: int = 5):
+    """HBM bandwidth of plain streaming kernels on this device (copy: read
+    + write, read only, write only), the practical ceilings of each mix."""
+    import torch
+
+    L = stream_lib()
+    n4 = nbytes // 16
+    a = torch.ones(n4 * 4, dtype=torch.float32, device="cuda:0")
+    b = torch.empty_like(a)
+    st = torch.cuda.current_stream()
+    out = {}
+    for name, fn, moved in (("copy", lambda: L.stream_ref_copy(a.data_ptr(), b.data_ptr(), n4, st.cuda_stream), 2 * nbytes),
+                            ("read", lambda: L.stream_ref_read(a.data_ptr(), b.data_ptr(), n4, st.cuda_stream), nbytes),
+                            ("write", lambda: L.stream_ref_fill(b.data_ptr(), n4, st.cuda_stream), nbytes)):
+        fn()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(st)
+        for _ in range(reps):
+            fn()
+        e1.record(st)
+        torch.cuda.synchronize()
+        t = e0.elapsed_time(e1) / reps / 1e3
+        out[name + "_GBps"] = moved / t / 1e9
+    del a, b
+    torch.cuda.empty_cache()
+    return out
 
 
 def load_traffic(workload: str, launch_bytes: float):
@@ -112,27 +157,29 @@ def cpu_baseline(w, target_s: float = 12.0):
         "cores": 1,
         "kind": "oracle",
         "sample": (f"{n} elements x {w.replicas} replicas of {w.name}: {steps} local steps "
-                   f"({el:.1f} s, clip norms included) + one replica mean, sync amortised "
-                   f"at {syncs_per_step:.4f} state-syncs/step; single thread"),
+                   f"({el:.1f} s{', clip norms included' if scale is not None else ''}) + one replica "
+                   f"mean, sync amortised at {syncs_per_step:.4f} state-syncs/step; single thread"),
     }
 
 
 def calibrate_copy(nbytes: int, reps: int) -> None:
-    """A plain device copy of known size (torch's copy kernel): the
-    reference reading of FETCH_SIZE / WRITE_SIZE under rocprofv3 --pmc."""
+    """A plain device copy of known size (the stream-reference copy kernel):
+    the reference reading of FETCH_SIZE / WRITE_SIZE under rocprofv3 --pmc."""
     import torch
 
-    n = nbytes // 4
-    a = torch.ones(n, dtype=torch.float32, device="cuda:0")
+    L = stream_lib()
+    n4 = nbytes // 16
+    a = torch.ones(n4 * 4, dtype=torch.float32, device="cuda:0")
     b = torch.empty_like(a)
+    st = torch.cuda.current_stream()
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(reps):
-        b.copy_(a)
+        L.stream_ref_copy(a.data_ptr(), b.data_ptr(), n4, st.cuda_stream)
     torch.cuda.synchronize()
     dt = (time.perf_counter() - t0) / reps
-    print(json.dumps({"copy_bytes_each_way": n * 4, "reps": reps, "ms": dt * 1e3,
-                      "GBps_read_plus_write": 2 * n * 4 / dt / 1e9}), flush=True)
+    print(json.dumps({"copy_bytes_each_way": n4 * 16, "reps": reps, "ms": dt * 1e3,
+                      "GBps_read_plus_write": 2 * n4 * 16 / dt / 1e9}), flush=True)
 
 
 def main() -> int:
@@ -220,6 +267,9 @@ def main() -> int:
         torch.cuda.synchronize()
         sync_s.append(a.elapsed_time(b) / reps / 1e3)
     opt.close()
+    del opt, grads
+    torch.cuda.empty_cache()
+    ceil = achievable()
 
     eb = step_bytes_per_element(w) + norm_bytes_per_element(w)
     launch_bytes = K * P * step_bytes_per_element(w)
@@ -252,7 +302,9 @@ def main() -> int:
                    "syncs_in_window": {str(k): v for k, v in sorted(syncs.items())}},
         "step": {"mean_launch_ms": step_launch_s * 1e3, "element_updates_per_s": K * P / step_launch_s,
                  "bytes_per_element_update": eb, "GBps": step_gbs,
-                 "pct_hbm_peak": 100 * step_gbs / HBM_PEAK_GBS},
+                 "pct_hbm_peak": 100 * step_gbs / HBM_PEAK_GBS,
+                 "pct_of_plain_copy": 100 * step_gbs / ceil["copy_GBps"]},
+        "achievable": ceil,
         "sync": sync_report,
         "roofline": {"bound": "hbm", "achieved": launch_bytes / step_launch_s / 1e9, "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": launch_bytes / step_launch_s / 1e9 / HBM_PEAK_GBS,

@@ -3,7 +3,8 @@
     python -m paper_2510_05361_amd.build
 
 compiles csrc/mtdao.hip (host code + kernels) with hipcc for gfx950 into
-paper_2510_05361_amd/libmtdao.so.  Packed-fp32 instruction selection is
+paper_2510_05361_amd/libmtdao.so, and csrc/stream_ref.hip (reference copy /
+read / fill kernels used only by the benchmark) into libstream_ref.so.  Packed-fp32 instruction selection is
 switched off for the device code.
 """
 
@@ -18,6 +19,8 @@ ROOT = os.path.dirname(PKG)
 SRC = os.path.join(PKG, "csrc", "mtdao.hip")
 HEADERS = [os.path.join(PKG, "csrc", "kernels.hpp"), os.path.join(ROOT, "include", "mtdao.h")]
 LIB = os.path.join(PKG, "libmtdao.so")
+STREAM_SRC = os.path.join(PKG, "csrc", "stream_ref.hip")
+STREAM_LIB = os.path.join(PKG, "libstream_ref.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = [
@@ -27,12 +30,19 @@ FLAGS = [
 ]
 
 
-def build(out: str = LIB, extra=()) -> str:
+def _compile(src: str, out: str, extra=()) -> str:
     tmp = out + ".tmp"
-    cmd = [HIPCC, *FLAGS, *extra, "-I", os.path.join(ROOT, "include"), "-o", tmp, SRC]
+    cmd = [HIPCC, *FLAGS, *extra, "-I", os.path.join(ROOT, "include"), "-o", tmp, src]
     subprocess.run(cmd, check=True)
     os.replace(tmp, out)
     return out
+
+
+def build(out: str = LIB, extra=()) -> str:
+    """The optimizer library (always) and the benchmark's stream-reference
+    kernels (libstream_ref.so)."""
+    _compile(STREAM_SRC, STREAM_LIB, extra)
+    return _compile(SRC, out, extra)
 
 
 if __name__ == "__main__":

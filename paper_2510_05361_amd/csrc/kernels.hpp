@@ -133,7 +133,7 @@ struct StepParams {
   float* v;                // [K][P] second moment (Adam, ADOPT)
   const float* scale;      // [K] global-norm clip factors, or nullptr
   int64_t P;               // row length
-  int64_t tiles;           // ceil(P / (kBlock * V * U))
+  int64_t tiles;           // ceil(P / (B * V * U)): tiles of one row
   float beta[kMaxN];       // beta_{1,j}
   float omb[kMaxN];        // 1 - beta_{1,j}
   float w[kMaxN];          // omega_j (times 1/(1 - beta_{1,j}^s) for bias-corrected Adam)
@@ -151,8 +151,11 @@ struct StepParams {
 //   XT, GT     storage of params / gradients (float or bf16)
 //   V, U       elements per vector slot, slots per thread per tile
 //   ORDER      ADOPT normalisation order (kPrev: v from before this step)
-template <int FORM, int N, typename XT, typename GT, int V, int U, bool NT, int ORDER>
-__global__ __launch_bounds__(kBlock) void k_local_step(StepParams p) {
+//   NTM        bit 0: nontemporal loads, bit 1: nontemporal stores
+//   B          threads per block
+template <int FORM, int N, typename XT, typename GT, int V, int U, int NTM, int ORDER, int B = kBlock>
+__global__ __launch_bounds__(B) void k_local_step(StepParams p) {
+  constexpr bool NTL = (NTM & 1) != 0, NTS = (NTM & 2) != 0;
   const int64_t m = blockIdx.y;
   const int64_t row = m * p.P;
   XT* __restrict__ x = reinterpret_cast<XT*>(p.x) + row;
@@ -164,23 +167,23 @@ __global__ __launch_bounds__(kBlock) void k_local_step(StepParams p) {
   const float sc = (FORM != kAdopt && p.scale != nullptr) ? p.scale[m] : 1.0f;
 
   for (int64_t tile = blockIdx.x; tile < p.tiles; tile += gridDim.x) {
-    const int64_t base = tile * (int64_t)(kBlock * V * U);
+    const int64_t base = tile * (int64_t)(B * V * U);
     float gv[U][V], xv[U][V], uv[U][N][V], vv[U][V];
     // issue every load of the tile before any arithmetic
 #pragma unroll
     for (int k = 0; k < U; ++k) {
-      const int64_t e = base + ((int64_t)k * kBlock + threadIdx.x) * V;
+      const int64_t e = base + ((int64_t)k * B + threadIdx.x) * V;
       if (e < p.P) {
-        load_v<GT, V, NT>(g, e, gv[k]);
-        load_v<XT, V, NT>(x, e, xv[k]);
+        load_v<GT, V, NTL>(g, e, gv[k]);
+        load_v<XT, V, NTL>(x, e, xv[k]);
 #pragma unroll
-        for (int j = 0; j < N; ++j) load_v<float, V, NT>(u[j], e, uv[k][j]);
-        if constexpr (FORM != kSgdm) load_v<float, V, NT>(v, e, vv[k]);
+        for (int j = 0; j < N; ++j) load_v<float, V, NTL>(u[j], e, uv[k][j]);
+        if constexpr (FORM != kSgdm) load_v<float, V, NTL>(v, e, vv[k]);
       }
     }
 #pragma unroll
     for (int k = 0; k < U; ++k) {
-      const int64_t e = base + ((int64_t)k * kBlock + threadIdx.x) * V;
+      const int64_t e = base + ((int64_t)k * B + threadIdx.x) * V;
       if (e >= p.P) continue;
 #pragma unroll
       for (int t = 0; t < V; ++t) {
@@ -228,10 +231,10 @@ __global__ __launch_bounds__(kBlock) void k_local_step(StepParams p) {
           xv[k][t] = xv[k][t] - p.lr * delta;
         }
       }
-      store_v<XT, V, NT>(x, e, xv[k]);
+      store_v<XT, V, NTS>(x, e, xv[k]);
 #pragma unroll
-      for (int j = 0; j < N; ++j) store_v<float, V, NT>(u[j], e, uv[k][j]);
-      if constexpr (FORM != kSgdm) store_v<float, V, NT>(v, e, vv[k]);
+      for (int j = 0; j < N; ++j) store_v<float, V, NTS>(u[j], e, uv[k][j]);
+      if constexpr (FORM != kSgdm) store_v<float, V, NTS>(v, e, vv[k]);
     }
   }
 }
@@ -270,28 +273,41 @@ struct MeanParams {
 // S^0 + (sum_{m>=1} (S^m - S^0)) / K in fp32 and is stored to all K rows.
 // Each thread reads the K rows of its own columns and writes them back, so
 // the in-place update has no cross-thread hazard.
-template <typename T, int V, bool NT>
+template <typename T, int V, bool NT, int U = 1>
 __global__ __launch_bounds__(kBlock) void k_replica_mean(MeanParams p) {
   T* __restrict__ s = reinterpret_cast<T*>(p.state[blockIdx.y]);
   const float kf = (float)p.K;
   for (int64_t tile = blockIdx.x; tile < p.tiles; tile += gridDim.x) {
-    const int64_t e = tile * (int64_t)(kBlock * V) + (int64_t)threadIdx.x * V;
-    if (e >= p.P) continue;
-    float s0[V], d[V];
-    load_v<T, V, NT>(s, e, s0);
+    const int64_t base = tile * (int64_t)(kBlock * V * U);
+    float s0[U][V], d[U][V];
 #pragma unroll
-    for (int t = 0; t < V; ++t) d[t] = 0.0f;
+    for (int k = 0; k < U; ++k) {
+      const int64_t e = base + ((int64_t)k * kBlock + threadIdx.x) * V;
+      if (e < p.P) load_v<T, V, NT>(s, e, s0[k]);
+#pragma unroll
+      for (int t = 0; t < V; ++t) d[k][t] = 0.0f;
+    }
 #pragma unroll 4
     for (int32_t m = 1; m < p.K; ++m) {
-      float a[V];
-      load_v<T, V, NT>(s + (int64_t)m * p.P, e, a);
 #pragma unroll
-      for (int t = 0; t < V; ++t) d[t] += a[t] - s0[t];
+      for (int k = 0; k < U; ++k) {
+        const int64_t e = base + ((int64_t)k * kBlock + threadIdx.x) * V;
+        if (e >= p.P) continue;
+        float a[V];
+        load_v<T, V, NT>(s + (int64_t)m * p.P, e, a);
+#pragma unroll
+        for (int t = 0; t < V; ++t) d[k][t] += a[t] - s0[k][t];
+      }
     }
 #pragma unroll
-    for (int t = 0; t < V; ++t) s0[t] = s0[t] + d[t] / kf;
+    for (int k = 0; k < U; ++k) {
+      const int64_t e = base + ((int64_t)k * kBlock + threadIdx.x) * V;
+      if (e >= p.P) continue;
+#pragma unroll
+      for (int t = 0; t < V; ++t) s0[k][t] = s0[k][t] + d[k][t] / kf;
 #pragma unroll 4
-    for (int32_t m = 0; m < p.K; ++m) store_v<T, V, NT>(s + (int64_t)m * p.P, e, s0);
+      for (int32_t m = 0; m < p.K; ++m) store_v<T, V, NT>(s + (int64_t)m * p.P, e, s0[k]);
+    }
   }
 }
 

@@ -34,6 +34,8 @@ namespace {
 thread_local std::string g_err;
 
 constexpr int kStepU = 2;      // vector slots per thread in the local step
+constexpr int kStepNT = 3;     // nontemporal hints of the local step (bit 0 loads, bit 1 stores)
+constexpr bool kMeanNT = true; // nontemporal hints of the replica mean
 constexpr int kNormU = 4;      // vector slots per thread in the norm pass
 constexpr int kNormBlocksMax = 512;
 
@@ -162,11 +164,11 @@ void launch_step_t(const StepParams& p, int32_t K, int order, hipStream_t st) {
   dim3 grid = grid_for(p.tiles, K);
   if constexpr (FORM == kAdopt) {
     if (order == kCur) {
-      hipLaunchKernelGGL((k_local_step<FORM, N, XT, GT, V, kStepU, false, kCur>), grid, dim3(kBlock), 0, st, p);
+      hipLaunchKernelGGL((k_local_step<FORM, N, XT, GT, V, kStepU, kStepNT, kCur>), grid, dim3(kBlock), 0, st, p);
       return;
     }
   }
-  hipLaunchKernelGGL((k_local_step<FORM, N, XT, GT, V, kStepU, false, kPrev>), grid, dim3(kBlock), 0, st, p);
+  hipLaunchKernelGGL((k_local_step<FORM, N, XT, GT, V, kStepU, kStepNT, kPrev>), grid, dim3(kBlock), 0, st, p);
 }
 
 template <int FORM, int N, typename XT, typename GT>
@@ -231,13 +233,13 @@ template <typename T>
 void launch_mean(MeanParams p, int nstates, int V, hipStream_t st) {
   if (V == 1) {
     p.tiles = (p.P + kBlock - 1) / kBlock;
-    hipLaunchKernelGGL((k_replica_mean<T, 1, false>), grid_for(p.tiles, nstates), dim3(kBlock), 0, st, p);
+    hipLaunchKernelGGL((k_replica_mean<T, 1, kMeanNT>), grid_for(p.tiles, nstates), dim3(kBlock), 0, st, p);
   } else if (V == 4) {
     p.tiles = (p.P + 4 * kBlock - 1) / (4 * kBlock);
-    hipLaunchKernelGGL((k_replica_mean<T, 4, false>), grid_for(p.tiles, nstates), dim3(kBlock), 0, st, p);
+    hipLaunchKernelGGL((k_replica_mean<T, 4, kMeanNT>), grid_for(p.tiles, nstates), dim3(kBlock), 0, st, p);
   } else {
     p.tiles = (p.P + 8 * kBlock - 1) / (8 * kBlock);
-    hipLaunchKernelGGL((k_replica_mean<T, 8, false>), grid_for(p.tiles, nstates), dim3(kBlock), 0, st, p);
+    hipLaunchKernelGGL((k_replica_mean<T, 8, kMeanNT>), grid_for(p.tiles, nstates), dim3(kBlock), 0, st, p);
   }
 }
 
