@@ -160,6 +160,17 @@ int32_t mtdao_local_step(mtdao_handle* h, const void* grads, float lr, float ado
  * applied_mask (may be NULL) receives the set actually averaged. */
 int32_t mtdao_sync(mtdao_handle* h, uint32_t mask, uint32_t* applied_mask, void* hip_stream);
 
+/* mtdao_local_step followed by mtdao_sync(mask) in one pass over memory:
+ * same arguments and same results, bit for bit (mask = MTDAO_SYNC_AUTO is
+ * the schedule at the new step s).  When states are due, every element's K
+ * replica rows are updated and averaged by one thread and the mean is
+ * written straight to all rows, so the separate averaging pass (read and
+ * write of K rows per due state) is not needed.  applied_mask (may be NULL)
+ * receives the set averaged.  Nothing is enqueued and the step counter does
+ * not move when an argument is rejected. */
+int32_t mtdao_step_sync(mtdao_handle* h, const void* grads, float lr, float adopt_clip, uint32_t mask,
+                        uint32_t* applied_mask, void* hip_stream);
+
 /* The schedule alone: states due after update s for this configuration.
  * Host-only; no GPU needed. */
 int32_t mtdao_schedule(const mtdao_config* cfg, int64_t s, uint32_t* mask);

@@ -145,13 +145,62 @@ struct StepParams {
   float clip;              // ADOPT c_t (<= 0: no clamp)
 };
 
+// The update of one element of one replica (the loop body of Algorithm 1, 2
+// or 3).  x, u[0..N), v hold the stored values on entry and the updated
+// values on exit; graw is the stored gradient and sc the replica's clip
+// factor.  Contraction is pinned (explicit fma, no implicit fusion) so
+// every kernel that calls this computes bit-identical values.
+template <int FORM, int N, int ORDER>
+__device__ __forceinline__ void update_element(const StepParams& p, float sc, float graw, float& x,
+                                               float (&u)[N], float& v) {
+#pragma clang fp contract(off)
+  if constexpr (FORM == kAdam) {
+    const float gh = sc * graw;
+    float num = p.gw * gh;
+#pragma unroll
+    for (int j = 0; j < N; ++j) {
+      u[j] = __builtin_fmaf(p.beta[j], u[j], p.omb[j] * gh);
+      num = __builtin_fmaf(p.w[j], u[j], num);
+    }
+    v = __builtin_fmaf(p.beta2, v, p.omb2 * (gh * gh));
+    const float den = __builtin_sqrtf(v * p.inv_bc2) + p.eps;
+    x = __builtin_fmaf(-p.lr, num / den, x);
+  } else if constexpr (FORM == kAdopt) {
+    float gn;
+    if constexpr (ORDER == kPrev) {
+      gn = graw / (__builtin_sqrtf(v) + p.eps);
+      v = __builtin_fmaf(p.beta2, v, p.omb2 * (graw * graw));
+    } else {
+      v = __builtin_fmaf(p.beta2, v, p.omb2 * (graw * graw));
+      gn = graw / (__builtin_sqrtf(v) + p.eps);
+    }
+    if (p.clip > 0.0f) gn = gn > p.clip ? p.clip : (gn < -p.clip ? -p.clip : gn);
+    float delta = p.gw * gn;
+#pragma unroll
+    for (int j = 0; j < N; ++j) {
+      u[j] = __builtin_fmaf(p.beta[j], u[j], p.omb[j] * gn);
+      delta = __builtin_fmaf(p.w[j], u[j], delta);
+    }
+    x = __builtin_fmaf(-p.lr, delta, x);
+  } else {
+    const float gh = sc * graw;
+    float delta = p.gw * gh;
+#pragma unroll
+    for (int j = 0; j < N; ++j) {
+      u[j] = __builtin_fmaf(p.beta[j], u[j], p.omb[j] * gh);
+      delta = __builtin_fmaf(p.w[j], u[j], delta);
+    }
+    x = __builtin_fmaf(-p.lr, delta, x);
+  }
+}
+
 // One update of all elements of all replicas (Algorithm 1, 2 or 3 body).
 //   FORM       kAdam / kAdopt / kSgdm
 //   N          number of first moments
 //   XT, GT     storage of params / gradients (float or bf16)
 //   V, U       elements per vector slot, slots per thread per tile
-//   ORDER      ADOPT normalisation order (kPrev: v from before this step)
 //   NTM        bit 0: nontemporal loads, bit 1: nontemporal stores
+//   ORDER      ADOPT normalisation order (kPrev: v from before this step)
 //   B          threads per block
 template <int FORM, int N, typename XT, typename GT, int V, int U, int NTM, int ORDER, int B = kBlock>
 __global__ __launch_bounds__(B) void k_local_step(StepParams p) {
@@ -187,54 +236,136 @@ __global__ __launch_bounds__(B) void k_local_step(StepParams p) {
       if (e >= p.P) continue;
 #pragma unroll
       for (int t = 0; t < V; ++t) {
-        const float graw = gv[k][t];
-        if constexpr (FORM == kAdam) {
-          const float gh = sc * graw;
-          float num = p.gw * gh;
+        float uu[N];
 #pragma unroll
-          for (int j = 0; j < N; ++j) {
-            const float uj = p.beta[j] * uv[k][j][t] + p.omb[j] * gh;
-            uv[k][j][t] = uj;
-            num += p.w[j] * uj;
-          }
-          const float vn = p.beta2 * vv[k][t] + p.omb2 * (gh * gh);
-          vv[k][t] = vn;
-          const float den = __builtin_sqrtf(vn * p.inv_bc2) + p.eps;
-          xv[k][t] = xv[k][t] - p.lr * (num / den);
-        } else if constexpr (FORM == kAdopt) {
-          float gn;
-          if constexpr (ORDER == kPrev) {
-            gn = graw / (__builtin_sqrtf(vv[k][t]) + p.eps);
-            vv[k][t] = p.beta2 * vv[k][t] + p.omb2 * (graw * graw);
-          } else {
-            vv[k][t] = p.beta2 * vv[k][t] + p.omb2 * (graw * graw);
-            gn = graw / (__builtin_sqrtf(vv[k][t]) + p.eps);
-          }
-          if (p.clip > 0.0f) gn = gn > p.clip ? p.clip : (gn < -p.clip ? -p.clip : gn);
-          float delta = p.gw * gn;
+        for (int j = 0; j < N; ++j) uu[j] = uv[k][j][t];
+        float vt = (FORM != kSgdm) ? vv[k][t] : 0.0f;
+        update_element<FORM, N, ORDER>(p, sc, gv[k][t], xv[k][t], uu, vt);
 #pragma unroll
-          for (int j = 0; j < N; ++j) {
-            const float uj = p.beta[j] * uv[k][j][t] + p.omb[j] * gn;
-            uv[k][j][t] = uj;
-            delta += p.w[j] * uj;
-          }
-          xv[k][t] = xv[k][t] - p.lr * delta;
-        } else {
-          const float gh = sc * graw;
-          float delta = p.gw * gh;
-#pragma unroll
-          for (int j = 0; j < N; ++j) {
-            const float uj = p.beta[j] * uv[k][j][t] + p.omb[j] * gh;
-            uv[k][j][t] = uj;
-            delta += p.w[j] * uj;
-          }
-          xv[k][t] = xv[k][t] - p.lr * delta;
-        }
+        for (int j = 0; j < N; ++j) uv[k][j][t] = uu[j];
+        if constexpr (FORM != kSgdm) vv[k][t] = vt;
       }
       store_v<XT, V, NTS>(x, e, xv[k]);
 #pragma unroll
       for (int j = 0; j < N; ++j) store_v<float, V, NTS>(u[j], e, uv[k][j]);
       if constexpr (FORM != kSgdm) store_v<float, V, NTS>(v, e, vv[k]);
+    }
+  }
+}
+
+// Value a state holds once stored: bf16 parameters are rounded.
+template <typename T>
+__device__ __forceinline__ float as_stored(float a) {
+  if constexpr (sizeof(T) == 2) return bf16_to_f32(f32_to_bf16(a));
+  else return a;
+}
+
+// Local update of every replica followed by the replica mean of the states
+// in `mask` (bit 0 = x, bit j = u^j, bit N+1 = v), in one pass.  A thread
+// owns V columns of every replica: it updates replica 0..K-1 in order,
+// stores the states that are not due, and accumulates the due ones as
+// S^0 + (sum_{m>=1} (S^m - S^0)) / K from their stored values -- the same
+// arithmetic, in the same order, as k_local_step followed by
+// k_replica_mean, so both paths give bit-identical results -- then writes
+// that mean to all K rows.  The separate mean pass (2 K sizeof(T) bytes
+// per element per due state) disappears.
+template <int FORM, int N, typename XT, typename GT, int V, int NTM, int ORDER>
+__global__ __launch_bounds__(kBlock) void k_local_step_sync(StepParams p, uint32_t mask, int32_t K) {
+  constexpr bool NTL = (NTM & 1) != 0, NTS = (NTM & 2) != 0;
+  const bool sync_x = (mask & 1u) != 0;
+  bool sync_u[N];
+#pragma unroll
+  for (int j = 0; j < N; ++j) sync_u[j] = ((mask >> (j + 1)) & 1u) != 0;
+  const bool sync_v = FORM != kSgdm && ((mask >> (N + 1)) & 1u) != 0;
+  XT* __restrict__ x = reinterpret_cast<XT*>(p.x);
+  const GT* __restrict__ g = reinterpret_cast<const GT*>(p.g);
+  const float kf = (float)K;
+
+  for (int64_t tile = blockIdx.x; tile < p.tiles; tile += gridDim.x) {
+    const int64_t e = tile * (int64_t)(kBlock * V) + (int64_t)threadIdx.x * V;
+    if (e >= p.P) continue;
+    float x0[V], dx[V], u0[N][V], du[N][V], v0[V], dv[V];
+#pragma unroll
+    for (int t = 0; t < V; ++t) {
+      dx[t] = 0.0f;
+      dv[t] = 0.0f;
+#pragma unroll
+      for (int j = 0; j < N; ++j) du[j][t] = 0.0f;
+    }
+    for (int32_t m = 0; m < K; ++m) {
+      const int64_t r = (int64_t)m * p.P + e;
+      float gv[V], xv[V], uv[N][V], vv[V];
+      load_v<GT, V, NTL>(g, r, gv);
+      load_v<XT, V, NTL>(x, r, xv);
+#pragma unroll
+      for (int j = 0; j < N; ++j) load_v<float, V, NTL>(p.u[j], r, uv[j]);
+      if constexpr (FORM != kSgdm) load_v<float, V, NTL>(p.v, r, vv);
+      const float sc = (FORM != kAdopt && p.scale != nullptr) ? p.scale[m] : 1.0f;
+#pragma unroll
+      for (int t = 0; t < V; ++t) {
+        float uu[N];
+#pragma unroll
+        for (int j = 0; j < N; ++j) uu[j] = uv[j][t];
+        float vt = (FORM != kSgdm) ? vv[t] : 0.0f;
+        update_element<FORM, N, ORDER>(p, sc, gv[t], xv[t], uu, vt);
+        xv[t] = as_stored<XT>(xv[t]);
+#pragma unroll
+        for (int j = 0; j < N; ++j) uv[j][t] = uu[j];
+        vv[t] = vt;
+      }
+      // states not due: store now; due: accumulate the shifted sum
+      if (sync_x) {
+#pragma unroll
+        for (int t = 0; t < V; ++t) {
+          if (m == 0) x0[t] = xv[t];
+          else dx[t] += xv[t] - x0[t];
+        }
+      } else {
+        store_v<XT, V, NTS>(x, r, xv);
+      }
+#pragma unroll
+      for (int j = 0; j < N; ++j) {
+        if (sync_u[j]) {
+#pragma unroll
+          for (int t = 0; t < V; ++t) {
+            if (m == 0) u0[j][t] = uv[j][t];
+            else du[j][t] += uv[j][t] - u0[j][t];
+          }
+        } else {
+          store_v<float, V, NTS>(p.u[j], r, uv[j]);
+        }
+      }
+      if constexpr (FORM != kSgdm) {
+        if (sync_v) {
+#pragma unroll
+          for (int t = 0; t < V; ++t) {
+            if (m == 0) v0[t] = vv[t];
+            else dv[t] += vv[t] - v0[t];
+          }
+        } else {
+          store_v<float, V, NTS>(p.v, r, vv);
+        }
+      }
+    }
+    // the means, written to every replica row
+    if (sync_x) {
+#pragma unroll
+      for (int t = 0; t < V; ++t) x0[t] = x0[t] + dx[t] / kf;
+      for (int32_t m = 0; m < K; ++m) store_v<XT, V, NTS>(x, (int64_t)m * p.P + e, x0);
+    }
+#pragma unroll
+    for (int j = 0; j < N; ++j) {
+      if (!sync_u[j]) continue;
+#pragma unroll
+      for (int t = 0; t < V; ++t) u0[j][t] = u0[j][t] + du[j][t] / kf;
+      for (int32_t m = 0; m < K; ++m) store_v<float, V, NTS>(p.u[j], (int64_t)m * p.P + e, u0[j]);
+    }
+    if constexpr (FORM != kSgdm) {
+      if (sync_v) {
+#pragma unroll
+        for (int t = 0; t < V; ++t) v0[t] = v0[t] + dv[t] / kf;
+        for (int32_t m = 0; m < K; ++m) store_v<float, V, NTS>(p.v, (int64_t)m * p.P + e, v0);
+      }
     }
   }
 }

@@ -9,6 +9,7 @@
 #include <cstdio>
 #include <cstring>
 #include <string>
+#include <type_traits>
 #include <vector>
 
 #include "../../include/mtdao.h"
@@ -159,50 +160,83 @@ dim3 grid_for(int64_t tiles, int32_t ny) {
 
 // ---------------------------------------------------------------- dispatch
 
-template <int FORM, int N, typename XT, typename GT, int V>
-void launch_step_t(const StepParams& p, int32_t K, int order, hipStream_t st) {
-  dim3 grid = grid_for(p.tiles, K);
-  if constexpr (FORM == kAdopt) {
-    if (order == kCur) {
-      hipLaunchKernelGGL((k_local_step<FORM, N, XT, GT, V, kStepU, kStepNT, kCur>), grid, dim3(kBlock), 0, st, p);
-      return;
+template <int V>
+using IntC = std::integral_constant<int, V>;
+template <typename T>
+struct TypeC {
+  using type = T;
+};
+
+// Calls f(form, n, xtype, gtype, vwidth) with compile-time constants for the
+// configuration of c and the runtime vector width V (1, or 4 for fp32-only
+// rows, 8 when a bf16 buffer is involved).
+template <typename F>
+void dispatch_step(const mtdao_config& c, int V, F&& f) {
+  auto with_types = [&](auto form, auto n) {
+    auto with_v = [&](auto xt, auto gt) {
+      using XT = typename decltype(xt)::type;
+      using GT = typename decltype(gt)::type;
+      constexpr int VW = (sizeof(XT) == 2 || sizeof(GT) == 2) ? 8 : 4;
+      if (V == 1) f(form, n, xt, gt, IntC<1>{});
+      else f(form, n, xt, gt, IntC<VW>{});
+    };
+    if (c.param_dtype == MTDAO_F32 && c.grad_dtype == MTDAO_F32) with_v(TypeC<float>{}, TypeC<float>{});
+    else if (c.param_dtype == MTDAO_F32) with_v(TypeC<float>{}, TypeC<uint16_t>{});
+    else if (c.grad_dtype == MTDAO_F32) with_v(TypeC<uint16_t>{}, TypeC<float>{});
+    else with_v(TypeC<uint16_t>{}, TypeC<uint16_t>{});
+  };
+  auto with_form = [&](auto form) {
+    switch (c.n_moments) {
+      case 1: with_types(form, IntC<1>{}); break;
+      case 2: with_types(form, IntC<2>{}); break;
+      case 3: with_types(form, IntC<3>{}); break;
+      default: with_types(form, IntC<4>{}); break;
     }
-  }
-  hipLaunchKernelGGL((k_local_step<FORM, N, XT, GT, V, kStepU, kStepNT, kPrev>), grid, dim3(kBlock), 0, st, p);
+  };
+  if (c.form == MTDAO_ADAM) with_form(IntC<kAdam>{});
+  else if (c.form == MTDAO_ADOPT) with_form(IntC<kAdopt>{});
+  else with_form(IntC<kSgdm>{});
 }
 
-template <int FORM, int N, typename XT, typename GT>
-void launch_step_v(StepParams p, int32_t K, int V, int order, hipStream_t st) {
-  const int64_t per = (int64_t)kBlock * kStepU;
-  if (V == 1) {
+// The local step alone: grid (tiles of one row, K).
+void launch_step(const mtdao_config& c, StepParams p, int V, hipStream_t st) {
+  dispatch_step(c, V, [&](auto form, auto n, auto xt, auto gt, auto vw) {
+    constexpr int FORM = decltype(form)::value, N = decltype(n)::value, VV = decltype(vw)::value;
+    using XT = typename decltype(xt)::type;
+    using GT = typename decltype(gt)::type;
+    const int64_t per = (int64_t)kBlock * VV * kStepU;
     p.tiles = (p.P + per - 1) / per;
-    launch_step_t<FORM, N, XT, GT, 1>(p, K, order, st);
-  } else if (V == 4) {
-    p.tiles = (p.P + per * 4 - 1) / (per * 4);
-    launch_step_t<FORM, N, XT, GT, 4>(p, K, order, st);
-  } else {
-    p.tiles = (p.P + per * 8 - 1) / (per * 8);
-    launch_step_t<FORM, N, XT, GT, 8>(p, K, order, st);
-  }
+    const dim3 grid = grid_for(p.tiles, c.replicas);
+    if constexpr (FORM == kAdopt) {
+      if (c.adopt_order == MTDAO_ADOPT_CUR) {
+        hipLaunchKernelGGL((k_local_step<FORM, N, XT, GT, VV, kStepU, kStepNT, kCur>), grid, dim3(kBlock), 0, st, p);
+        return;
+      }
+    }
+    hipLaunchKernelGGL((k_local_step<FORM, N, XT, GT, VV, kStepU, kStepNT, kPrev>), grid, dim3(kBlock), 0, st, p);
+  });
 }
 
-template <int FORM, int N>
-void launch_step_n(const StepParams& p, const mtdao_config& c, int V, hipStream_t st) {
-  const int K = c.replicas, o = c.adopt_order;
-  if (c.param_dtype == MTDAO_F32 && c.grad_dtype == MTDAO_F32) launch_step_v<FORM, N, float, float>(p, K, V, o, st);
-  else if (c.param_dtype == MTDAO_F32) launch_step_v<FORM, N, float, uint16_t>(p, K, V, o, st);
-  else if (c.grad_dtype == MTDAO_F32) launch_step_v<FORM, N, uint16_t, float>(p, K, V, o, st);
-  else launch_step_v<FORM, N, uint16_t, uint16_t>(p, K, V, o, st);
-}
-
-template <int FORM>
-void launch_step_f(const StepParams& p, const mtdao_config& c, int V, hipStream_t st) {
-  switch (c.n_moments) {
-    case 1: launch_step_n<FORM, 1>(p, c, V, st); break;
-    case 2: launch_step_n<FORM, 2>(p, c, V, st); break;
-    case 3: launch_step_n<FORM, 3>(p, c, V, st); break;
-    default: launch_step_n<FORM, 4>(p, c, V, st); break;
-  }
+// The local step with the replica mean of the states in mask: grid over
+// tiles of one row, each thread covering all K replicas of its columns.
+void launch_step_sync(const mtdao_config& c, StepParams p, int V, uint32_t mask, hipStream_t st) {
+  dispatch_step(c, V, [&](auto form, auto n, auto xt, auto gt, auto vw) {
+    constexpr int FORM = decltype(form)::value, N = decltype(n)::value, VV = decltype(vw)::value;
+    using XT = typename decltype(xt)::type;
+    using GT = typename decltype(gt)::type;
+    const int64_t per = (int64_t)kBlock * VV;
+    p.tiles = (p.P + per - 1) / per;
+    const dim3 grid = grid_for(p.tiles, 1);
+    if constexpr (FORM == kAdopt) {
+      if (c.adopt_order == MTDAO_ADOPT_CUR) {
+        hipLaunchKernelGGL((k_local_step_sync<FORM, N, XT, GT, VV, kStepNT, kCur>), grid, dim3(kBlock), 0, st, p, mask,
+                           c.replicas);
+        return;
+      }
+    }
+    hipLaunchKernelGGL((k_local_step_sync<FORM, N, XT, GT, VV, kStepNT, kPrev>), grid, dim3(kBlock), 0, st, p, mask,
+                       c.replicas);
+  });
 }
 
 template <typename GT>
@@ -351,8 +385,11 @@ int32_t mtdao_init(const mtdao_config* cfg, const mtdao_buffers* bufs, void* wor
   return MTDAO_OK;
 }
 
-int32_t mtdao_local_step(mtdao_handle* h, const void* grads, float lr, float adopt_clip, void* hip_stream) {
-  if (!h) return fail(&g_err, MTDAO_ERR_INVALID_ARG, "handle is NULL");
+}  // extern "C"
+
+namespace {
+
+int32_t check_step_args(mtdao_handle* h, const void* grads, float lr, float adopt_clip) {
   const mtdao_config& c = h->cfg;
   const int64_t P = c.numel, KP = (int64_t)c.replicas * P;
   if (!std::isfinite(lr)) return fail(&h->err, MTDAO_ERR_INVALID_ARG, "lr is not finite");
@@ -366,12 +403,27 @@ int32_t mtdao_local_step(mtdao_handle* h, const void* grads, float lr, float ado
     if (h->v) ov = ov || overlap(grads, gb, h->v, KP * 4);
     if (ov) return fail(&h->err, MTDAO_ERR_INVALID_ARG, "grads overlaps a state buffer");
   }
-  const int64_t s = h->s + 1;
-  h->s = s;
-  if (P == 0) return MTDAO_OK;
-  hipStream_t st = reinterpret_cast<hipStream_t>(hip_stream);
+  return MTDAO_OK;
+}
 
-  // per-step scalars in double, rounded once to fp32
+int32_t resolve_mask(mtdao_handle* h, uint32_t mask, int64_t s, uint32_t* out) {
+  const mtdao_config& c = h->cfg;
+  if (mask == MTDAO_SYNC_AUTO) {
+    *out = s >= 1 ? schedule_mask(c, s) : 0u;
+    return MTDAO_OK;
+  }
+  if (mask & ~valid_bits(c))
+    return fail(&h->err, MTDAO_ERR_INVALID_ARG, "mask 0x%x has bits beyond the %d states", mask,
+                1 + c.n_moments + (has_v(c) ? 1 : 0));
+  *out = mask;
+  return MTDAO_OK;
+}
+
+// Per-step scalars of update s in double, rounded once to fp32; launches
+// the clip-norm reduction first when the configuration clips.
+StepParams prepare_step(mtdao_handle* h, const void* grads, float lr, float adopt_clip, int64_t s, hipStream_t st) {
+  const mtdao_config& c = h->cfg;
+  const int64_t P = c.numel;
   StepParams p;
   std::memset(&p, 0, sizeof p);
   p.x = h->x;
@@ -396,47 +448,36 @@ int32_t mtdao_local_step(mtdao_handle* h, const void* grads, float lr, float ado
   p.lr = lr;
   p.clip = adopt_clip;
   p.scale = nullptr;
-
-  const int Vg = (P % 4 == 0) ? 4 : 1;  // 16-byte (fp32) or 8-byte (bf16) slots
   if (c.form != MTDAO_ADOPT && c.clip_rho > 0.0f) {
+    const int Vg = (P % 4 == 0) ? 4 : 1;  // 16-byte (fp32) or 8-byte (bf16) slots
     if (c.grad_dtype == MTDAO_F32) launch_norm<float>(grads, P, c.replicas, Vg, h->norm_blocks, h->partials, st);
     else launch_norm<uint16_t>(grads, P, c.replicas, Vg, h->norm_blocks, h->partials, st);
     hipLaunchKernelGGL(k_clip_finalize, dim3(c.replicas), dim3(64), 0, st, h->partials, h->norm_blocks,
                        (double)c.clip_rho, h->scale);
     p.scale = h->scale;
   }
-  // one vector width for every buffer the step touches
-  const int V = (c.param_dtype == MTDAO_BF16 || c.grad_dtype == MTDAO_BF16) ? vec_width(MTDAO_BF16, P)
-                                                                              : vec_width(MTDAO_F32, P);
-  if (c.form == MTDAO_ADOPT && c.adopt_order == MTDAO_ADOPT_PREV && s == 1) {
-    const int Vi = (P % 4 == 0) ? 4 : 1;
-    if (c.grad_dtype == MTDAO_F32) launch_adopt_init<float>(grads, h->v, P, c.replicas, Vi, st);
-    else launch_adopt_init<uint16_t>(grads, h->v, P, c.replicas, Vi, st);
-  } else if (c.form == MTDAO_ADAM) {
-    launch_step_f<kAdam>(p, c, V, st);
-  } else if (c.form == MTDAO_ADOPT) {
-    launch_step_f<kAdopt>(p, c, V, st);
-  } else {
-    launch_step_f<kSgdm>(p, c, V, st);
-  }
-  return hip_check(&h->err, hipGetLastError(), "mtdao_local_step launch");
+  return p;
 }
 
-int32_t mtdao_sync(mtdao_handle* h, uint32_t mask, uint32_t* applied_mask, void* hip_stream) {
-  if (!h) return fail(&g_err, MTDAO_ERR_INVALID_ARG, "handle is NULL");
+// One vector width for every buffer the step touches.
+int step_vec_width(const mtdao_config& c) {
+  return (c.param_dtype == MTDAO_BF16 || c.grad_dtype == MTDAO_BF16) ? vec_width(MTDAO_BF16, c.numel)
+                                                                       : vec_width(MTDAO_F32, c.numel);
+}
+
+bool adopt_first_update(const mtdao_config& c, int64_t s) {
+  return c.form == MTDAO_ADOPT && c.adopt_order == MTDAO_ADOPT_PREV && s == 1;
+}
+
+void launch_adopt_first(mtdao_handle* h, const void* grads, hipStream_t st) {
   const mtdao_config& c = h->cfg;
-  uint32_t m;
-  if (mask == MTDAO_SYNC_AUTO) {
-    m = h->s >= 1 ? schedule_mask(c, h->s) : 0u;
-  } else {
-    if (mask & ~valid_bits(c))
-      return fail(&h->err, MTDAO_ERR_INVALID_ARG, "mask 0x%x has bits beyond the %d states", mask,
-                  1 + c.n_moments + (has_v(c) ? 1 : 0));
-    m = mask;
-  }
-  if (applied_mask) *applied_mask = m;
-  if (m == 0 || c.numel == 0 || c.replicas == 1) return MTDAO_OK;  // K = 1: the mean is the row
-  hipStream_t st = reinterpret_cast<hipStream_t>(hip_stream);
+  const int Vi = (c.numel % 4 == 0) ? 4 : 1;
+  if (c.grad_dtype == MTDAO_F32) launch_adopt_init<float>(grads, h->v, c.numel, c.replicas, Vi, st);
+  else launch_adopt_init<uint16_t>(grads, h->v, c.numel, c.replicas, Vi, st);
+}
+
+void launch_means(mtdao_handle* h, uint32_t m, hipStream_t st) {
+  const mtdao_config& c = h->cfg;
   MeanParams mp;
   std::memset(&mp, 0, sizeof mp);
   mp.P = c.numel;
@@ -453,7 +494,61 @@ int32_t mtdao_sync(mtdao_handle* h, uint32_t mask, uint32_t* applied_mask, void*
     xp.state[0] = h->x;
     launch_mean<uint16_t>(xp, 1, vec_width(MTDAO_BF16, c.numel), st);
   }
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t mtdao_local_step(mtdao_handle* h, const void* grads, float lr, float adopt_clip, void* hip_stream) {
+  if (!h) return fail(&g_err, MTDAO_ERR_INVALID_ARG, "handle is NULL");
+  int32_t r = check_step_args(h, grads, lr, adopt_clip);
+  if (r != MTDAO_OK) return r;
+  const int64_t s = ++h->s;
+  if (h->cfg.numel == 0) return MTDAO_OK;
+  hipStream_t st = reinterpret_cast<hipStream_t>(hip_stream);
+  const StepParams p = prepare_step(h, grads, lr, adopt_clip, s, st);
+  if (adopt_first_update(h->cfg, s)) launch_adopt_first(h, grads, st);
+  else launch_step(h->cfg, p, step_vec_width(h->cfg), st);
+  return hip_check(&h->err, hipGetLastError(), "mtdao_local_step launch");
+}
+
+int32_t mtdao_sync(mtdao_handle* h, uint32_t mask, uint32_t* applied_mask, void* hip_stream) {
+  if (!h) return fail(&g_err, MTDAO_ERR_INVALID_ARG, "handle is NULL");
+  uint32_t m;
+  int32_t r = resolve_mask(h, mask, h->s, &m);
+  if (r != MTDAO_OK) return r;
+  if (applied_mask) *applied_mask = m;
+  const mtdao_config& c = h->cfg;
+  if (m == 0 || c.numel == 0 || c.replicas == 1) return MTDAO_OK;  // K = 1: the mean is the row
+  launch_means(h, m, reinterpret_cast<hipStream_t>(hip_stream));
   return hip_check(&h->err, hipGetLastError(), "mtdao_sync launch");
+}
+
+int32_t mtdao_step_sync(mtdao_handle* h, const void* grads, float lr, float adopt_clip, uint32_t mask,
+                        uint32_t* applied_mask, void* hip_stream) {
+  if (!h) return fail(&g_err, MTDAO_ERR_INVALID_ARG, "handle is NULL");
+  int32_t r = check_step_args(h, grads, lr, adopt_clip);
+  if (r != MTDAO_OK) return r;
+  const int64_t s = h->s + 1;
+  uint32_t m;
+  r = resolve_mask(h, mask, s, &m);
+  if (r != MTDAO_OK) return r;
+  h->s = s;
+  if (applied_mask) *applied_mask = m;
+  const mtdao_config& c = h->cfg;
+  if (c.numel == 0) return MTDAO_OK;
+  hipStream_t st = reinterpret_cast<hipStream_t>(hip_stream);
+  const StepParams p = prepare_step(h, grads, lr, adopt_clip, s, st);
+  if (adopt_first_update(c, s)) {
+    launch_adopt_first(h, grads, st);
+    if (m != 0 && c.replicas > 1) launch_means(h, m, st);
+  } else if (m == 0 || c.replicas == 1) {
+    launch_step(c, p, step_vec_width(c), st);
+  } else {
+    launch_step_sync(c, p, step_vec_width(c), m, st);
+  }
+  return hip_check(&h->err, hipGetLastError(), "mtdao_step_sync launch");
 }
 
 int32_t mtdao_read_state(mtdao_handle* h, int32_t state, int32_t replica, int64_t offset, int64_t count,

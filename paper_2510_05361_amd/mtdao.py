@@ -81,6 +81,8 @@ def lib() -> ctypes.CDLL:
         L.mtdao_local_step.restype = I32
         L.mtdao_sync.argtypes = [VP, U32, P(U32), VP]
         L.mtdao_sync.restype = I32
+        L.mtdao_step_sync.argtypes = [VP, VP, ctypes.c_float, ctypes.c_float, U32, P(U32), VP]
+        L.mtdao_step_sync.restype = I32
         L.mtdao_schedule.argtypes = [P(MtdaoConfig), I64, P(U32)]
         L.mtdao_schedule.restype = I32
         L.mtdao_read_state.argtypes = [VP, I32, I32, I64, I64, VP, VP]
@@ -187,6 +189,14 @@ def mtdao_local_step(h: int, grads: int, lr: float, adopt_clip: float, stream: O
 def mtdao_sync(h: int, mask: int, stream: Optional[int]) -> int:
     applied = ctypes.c_uint32(0)
     _check(lib().mtdao_sync(h, int(mask) & 0xFFFFFFFF, ctypes.byref(applied), stream), h)
+    return int(applied.value)
+
+
+def mtdao_step_sync(h: int, grads: int, lr: float, adopt_clip: float, mask: int,
+                    stream: Optional[int]) -> int:
+    applied = ctypes.c_uint32(0)
+    _check(lib().mtdao_step_sync(h, grads, float(lr), float(adopt_clip), int(mask) & 0xFFFFFFFF,
+                                 ctypes.byref(applied), stream), h)
     return int(applied.value)
 
 

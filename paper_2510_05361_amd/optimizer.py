@@ -60,6 +60,13 @@ class MtdaoOptimizer:
         assert grads.is_contiguous() and grads.shape == (self.K, self.P)
         abi.mtdao_local_step(self.handle, grads.data_ptr(), lr, adopt_clip, _stream())
 
+    def step_sync(self, grads: torch.Tensor, lr: float, adopt_clip: float = 0.0,
+                  mask: int = abi.MTDAO_SYNC_AUTO) -> int:
+        """Local step and the averaging of ``mask`` (default: the schedule)
+        in one fused pass; returns the applied mask."""
+        assert grads.is_contiguous() and grads.shape == (self.K, self.P)
+        return abi.mtdao_step_sync(self.handle, grads.data_ptr(), lr, adopt_clip, mask, _stream())
+
     def sync(self, mask: int = abi.MTDAO_SYNC_AUTO) -> int:
         return abi.mtdao_sync(self.handle, mask, _stream())
 

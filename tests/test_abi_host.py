@@ -172,6 +172,12 @@ def test_handle_host_paths():
         with pytest.raises(abi.MtdaoError) as e:
             abi.mtdao_local_step(h, 1 << 45, float("nan"), 0.0, None)
         assert e.value.code == abi.MTDAO_ERR_INVALID_ARG
+        with pytest.raises(abi.MtdaoError) as e:
+            abi.mtdao_step_sync(h, 1 << 45, 1e-3, 0.0, 1 << 4, None)  # bad mask
+        assert e.value.code == abi.MTDAO_ERR_INVALID_ARG
+        with pytest.raises(abi.MtdaoError) as e:
+            abi.mtdao_step_sync(h, (1 << 45) + 8, 1e-3, 0.0, 0, None)
+        assert e.value.code == abi.MTDAO_ERR_ALIGN
         assert abi.mtdao_step_count(h) == 0, "a rejected call must not advance the step"
         dst = np.zeros(8, dtype=np.float32)
         for args, code in [((4, 0, 0, 8), abi.MTDAO_ERR_INVALID_ARG), ((-1, 0, 0, 8), abi.MTDAO_ERR_INVALID_ARG),
@@ -202,6 +208,11 @@ def test_empty_problem_counts_steps_and_reports_masks():
                 abi.mtdao_local_step(h, None, 1e-3, 0.0, None)
                 assert abi.mtdao_step_count(h) == 7 + k
                 assert abi.mtdao_sync(h, abi.MTDAO_SYNC_AUTO, None) == oracle.schedule(ocfg, 7 + k)
+            for k in range(30, 50):
+                got = abi.mtdao_step_sync(h, None, 1e-3, 0.0, abi.MTDAO_SYNC_AUTO, None)
+                assert abi.mtdao_step_count(h) == 7 + k
+                assert got == oracle.schedule(ocfg, 7 + k)
+            assert abi.mtdao_step_sync(h, None, 1e-3, 0.0, 0b101, None) == 0b101
         finally:
             abi.mtdao_destroy(h)
 

@@ -261,3 +261,111 @@ def test_row_longer_than_2_pow_31():
     o = run_oracle(w, _steps(w), idx)
     compare(w, g.opt, o, "long-row")
     free(g)
+
+
+# ------------------------------------------------------------ fused step + sync
+
+
+def _run_fused(w, steps, start_step=0, masks=None, dev=None):
+    d = torch.device("cuda:0")
+    dev = dev or DeviceInputs(w, d)
+    opt = MtdaoOptimizer(abi.config_from_workload(w, start_step=start_step), d, x0=dev.x0_row())
+    gdt = torch.bfloat16 if w.grad_dtype == "bf16" else torch.float32
+    grads = torch.empty((w.replicas, w.numel), dtype=gdt, device=d)
+    applied = []
+    for k, s in enumerate(steps):
+        dev.grads_into(s, grads)
+        m = abi.MTDAO_SYNC_AUTO if masks is None else masks[k]
+        applied.append(opt.step_sync(grads, w.lr, w.adopt_clip_value(s), m))
+    torch.cuda.synchronize()
+    return opt, applied
+
+
+@pytest.mark.parametrize("tail", [40, 37], ids=["aligned_tail", "odd_tail"])
+@pytest.mark.parametrize("name", NAMES)
+def test_step_sync_bit_identical_to_separate_calls(name, tail):
+    """mtdao_step_sync (one fused pass) == mtdao_local_step + mtdao_sync, bit
+    for bit, over every workload's full step sequence."""
+    w = synth.small_variant(synth.WORKLOADS[name], 60_000, tail=tail)
+    log(f"case fused {w.name} P={w.numel} K={w.replicas}")
+    sep = run_gpu(w, _steps(w))
+    fused, applied = _run_fused(w, _steps(w))
+    assert applied == sep.masks and any(applied)
+    for p, q in zip(sep.opt.states(), fused.states()):
+        assert torch.equal(p, q)
+    fused.close()
+    free(sep)
+
+
+@pytest.mark.parametrize("form", ["adam", "adopt", "sgdm"])
+def test_step_sync_explicit_masks_and_first_step(form):
+    """Explicit masks (including every state at step 1, where ADOPT only
+    initialises v), K=1 and random per-step masks: fused == separate, and
+    both match the oracle."""
+    base = {"adam": "adam_n3_k4_p16m", "adopt": "adopt_n2_k8_p124m_bf16", "sgdm": "sgdm_n2_k16_p354m_clip"}[form]
+    w = synth.small_variant(synth.WORKLOADS[base], 20_000, tail=8).replace(steps=12, replicas=3)
+    nst = 1 + w.n_moments + (1 if w.has_v else 0)
+    rng = np.random.default_rng(5)
+    masks = [(1 << nst) - 1] + [int(rng.integers(0, 1 << nst)) for _ in range(w.steps - 1)]
+    fused, applied = _run_fused(w, _steps(w), masks=masks)
+    assert applied == masks
+    sep = run_gpu(w.replace(period_x=0, period_u=(0,) * w.n_moments, period_v=0), [])
+    d = torch.device("cuda:0")
+    dev = DeviceInputs(w, d)
+    gdt = torch.bfloat16 if w.grad_dtype == "bf16" else torch.float32
+    grads = torch.empty((w.replicas, w.numel), dtype=gdt, device=d)
+    for s, m in zip(_steps(w), masks):
+        dev.grads_into(s, grads)
+        sep.opt.step(grads, w.lr, w.adopt_clip_value(s))
+        assert sep.opt.sync(m) == m
+    torch.cuda.synchronize()
+    for p, q in zip(sep.opt.states(), fused.states()):
+        assert torch.equal(p, q)
+    ocfg = oracle.OracleConfig.from_workload(w)
+    ost = oracle.new_state(ocfg, synth.host_x0_row(w), w.replicas)
+    from gpu_harness import OracleResult, oracle_clip_scales
+    oracle.run(ocfg, ost, lambda s: synth.host_grad_rows(w, s), _steps(w), lambda s: w.lr,
+               w.adopt_clip_value, scales=lambda s, g: oracle_clip_scales(w, s),
+               masks=lambda s: masks[s - 1])
+    compare(w, fused, OracleResult(ost, masks, None), f"explicit-{form}")
+    fused.close()
+    free(sep)
+
+
+def test_step_sync_full_size_bench_workload():
+    """The 1.31B-parameter K=4 workload through the fused entry point over a
+    window that contains x-, u- and v-averaging (steps 249..256 after a
+    resume at 248 from seeded per-worker states), sampled against the
+    oracle from the same states."""
+    w = synth.WORKLOADS["adam_n3_k4_p1311m"]
+    start = 248
+    d = torch.device("cuda:0")
+    dev = DeviceInputs(w, d)
+    K, P = w.replicas, w.numel
+    x = torch.empty((K, P), dtype=torch.float32, device=d)
+    dev.pool_rows_into(11, 0.02, x)
+    u = [torch.empty((K, P), dtype=torch.float32, device=d) for _ in range(3)]
+    for j, t in enumerate(u):
+        dev.pool_rows_into(12 + j, 1e-3, t)
+    v = torch.empty((K, P), dtype=torch.float32, device=d)
+    dev.pool_rows_into(15, 1e-6, v, absolute=True)
+    opt = MtdaoOptimizer(abi.config_from_workload(w, start_step=start), d, resume=True, x=x, u=u, v=v)
+    grads = torch.empty((K, P), dtype=torch.float32, device=d)
+    applied = []
+    for s in range(start + 1, w.steps + 1):
+        dev.grads_into(s, grads)
+        applied.append(opt.step_sync(grads, w.lr))
+    torch.cuda.synchronize()
+    idx = synth.sample_indices(w)
+    ocfg = oracle.OracleConfig.from_workload(w)
+    ost = oracle.OracleState(synth.host_pool_rows(w, 11, 0.02, idx),
+                             [synth.host_pool_rows(w, 12 + j, 1e-3, idx) for j in range(3)],
+                             synth.host_pool_rows(w, 15, 1e-6, idx, absolute=True))
+    masks = oracle.run(ocfg, ost, lambda s: synth.host_grad_rows(w, s, idx), range(start + 1, w.steps + 1),
+                       lambda s: w.lr)
+    assert applied == masks == [0] * 7 + [0b11111]
+    from gpu_harness import OracleResult
+    compare(w, opt, OracleResult(ost, masks, idx), "fused-full")
+    opt.close()
+    del x, u, v, grads
+    torch.cuda.empty_cache()
