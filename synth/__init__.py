@@ -18,6 +18,7 @@ from .workloads import (  # noqa: F401
     grad_pool,
     x_pool,
     host_grad_rows,
+    host_pool_rows,
     host_x0_row,
     f32_to_bf16_bits,
     bf16_bits_to_f32,

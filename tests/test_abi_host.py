@@ -238,6 +238,11 @@ def test_device_generator_matches_host_generator():
         hx = synth.host_x0_row(w)
         xd = x0.view(torch.int16).numpy().view(np.uint16) if w.param_dtype == "bf16" else x0.numpy()
         assert np.array_equal(xd, hx), w.name
+        for stream, scale, absolute in [(11, 0.02, False), (15, 1e-6, True)]:
+            t = torch.empty((w.replicas, w.numel), dtype=torch.float32)
+            dev.pool_rows_into(stream, scale, t, absolute=absolute)
+            assert np.array_equal(t.numpy(), synth.host_pool_rows(w, stream, scale, np.arange(w.numel),
+                                                                  absolute=absolute))
         idx = synth.sample_indices(w, 500)
         assert np.array_equal(synth.host_grad_rows(w, 5, idx), synth.host_grad_rows(w, 5)[:, idx])
 
