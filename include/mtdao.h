@@ -76,6 +76,16 @@ enum { MTDAO_ADAM = 0, MTDAO_ADOPT = 1, MTDAO_SGDM = 2 };
 enum { MTDAO_F32 = 0, MTDAO_BF16 = 1 };
 /* ADOPT normalisation order */
 enum { MTDAO_ADOPT_PREV = 0, MTDAO_ADOPT_CUR = 1 };
+/* Where the averaging of a first moment sits within a step:
+ *   MTDAO_SYNC_AFTER_STEP      the step uses each worker's own u^j; the mean
+ *                              is the base of the next step (Algorithms 1-3)
+ *   MTDAO_SYNC_MOMENTA_IN_STEP the mean of a due u^j replaces it before this
+ *                              step's direction uses it (the probabilistic
+ *                              variant, Algorithm 4; SGDM form only).  Its
+ *                              moment averaging happens inside
+ *                              mtdao_step_sync; mtdao_sync then accepts only
+ *                              the x bit. */
+enum { MTDAO_SYNC_AFTER_STEP = 0, MTDAO_SYNC_MOMENTA_IN_STEP = 1 };
 /* status codes */
 enum {
   MTDAO_OK = 0,
@@ -110,6 +120,7 @@ typedef struct mtdao_config {
   int64_t numel;            /* P >= 0: elements per replica                          */
   int32_t n_tensors;        /* entries of tensor_numel (0: one tensor of P elements) */
   const int64_t* tensor_numel; /* host array, sums to P; copied by mtdao_init        */
+  int32_t sync_order;       /* MTDAO_SYNC_AFTER_STEP (default) / _MOMENTA_IN_STEP    */
 } mtdao_config;
 
 /* Device state buffers (caller-owned, [K][P] each, see layout above). */

@@ -85,6 +85,10 @@ def lib():
                                         ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                                         ctypes.c_int64, ctypes.c_int64]
         L.oracle_replica_mean.restype = None
+        L.oracle_sgdm_prob_step.restype = None
+        L.oracle_sgdm_prob_step.argtypes = [ctypes.POINTER(_Cfg), ctypes.c_float, ctypes.c_uint32,
+                                            ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                            ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64]
         L.oracle_replica_mean.argtypes = [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64,
                                           ctypes.c_int64]
         _lib = L
@@ -216,6 +220,38 @@ def local_step(cfg: OracleConfig, st: OracleState, g: np.ndarray, s: int, lr: fl
     lib().oracle_local_step(ctypes.byref(c), int(s), float(lr), float(clip_c), sc, _ptr(st.x),
                             ctypes.cast(uarr, ctypes.c_void_p),
                             None if st.v is None else _ptr(st.v), _ptr(g), K, P)
+
+
+def sgdm_prob_step(cfg: OracleConfig, st: OracleState, g: np.ndarray, lr: float, mask: int,
+                   scale: Optional[np.ndarray] = None) -> None:
+    """One step of the probabilistic SGDM variant (Algorithm 4) with this
+    step's averaging events ``mask``; averaged moments feed this step's
+    update."""
+    assert cfg.form == "sgdm"
+    K, P = st.x.shape
+    g = np.ascontiguousarray(g, dtype=_NP_DTYPE[_DTYPES[cfg.g_dtype]])
+    uarr = (ctypes.c_void_p * MAX_N)(*([_ptr(a) for a in st.u] + [None] * (MAX_N - cfg.n)))
+    sc = None
+    if scale is not None:
+        scale = np.ascontiguousarray(scale, dtype=np.float64)
+        sc = _ptr(scale)
+    c = cfg.c_struct()
+    lib().oracle_sgdm_prob_step(ctypes.byref(c), float(lr), int(mask) & 0xFFFFFFFF, sc, _ptr(st.x),
+                                ctypes.cast(uarr, ctypes.c_void_p), _ptr(g), K, P)
+
+
+def run_probabilistic(cfg: OracleConfig, st: OracleState, grads: Callable[[int], np.ndarray],
+                      steps: Sequence[int], lr: Callable[[int], float], masks: Callable[[int], int],
+                      scales: Optional[Callable[[int, np.ndarray], Optional[np.ndarray]]] = None) -> List[int]:
+    """Algorithm 4 over global steps ``steps`` with caller-drawn events."""
+    applied = []
+    for s in steps:
+        g = grads(s)
+        sc = scales(s, g) if scales is not None else clip_scales(cfg, g)
+        m = masks(s)
+        sgdm_prob_step(cfg, st, g, lr(s), m, sc)
+        applied.append(m)
+    return applied
 
 
 def replica_mean(a: np.ndarray, dtype: str) -> None:

@@ -241,6 +241,57 @@ void oracle_local_step(const oracle_cfg* c, int64_t s, float lr, float clip_c, c
   }
 }
 
+/* ------------------------------------------- probabilistic variant */
+
+/*
+ * One step of the probabilistic SGDM variant (Algorithm 4) given this
+ * step's averaging events in mask (bit 0 = x, bit j = u^j), which the
+ * caller draws: for every element, each first moment of every worker is
+ * updated and, when its event fires, replaced by its worker mean BEFORE the
+ * update direction uses it; x of every worker is updated with that
+ * direction and, when its event fires, replaced by its worker mean.
+ * The gradient term (1 - sum omega) is kept for generality (Algorithm 4
+ * has sum omega = 1, so it is zero there); scale as in oracle_local_step.
+ */
+void oracle_sgdm_prob_step(const oracle_cfg* c, float lr, uint32_t mask, const double* scale, void* x,
+                           void* const* u, const void* g, int64_t K, int64_t P) {
+  const int32_t n = c->n;
+  double beta[OR_MAX_N], omega[OR_MAX_N], omega_sum = 0.0;
+  for (int32_t j = 0; j < n; ++j) {
+    beta[j] = (double)c->beta1[j];
+    omega[j] = (double)c->omega[j];
+    omega_sum += omega[j];
+  }
+  const double g_weight = 1.0 - omega_sum;
+  const double eta = (double)lr;
+  for (int64_t p = 0; p < P; ++p) {
+    for (int32_t j = 0; j < n; ++j) {
+      for (int64_t m = 0; m < K; ++m) {
+        const int64_t i = m * P + p;
+        const double gh = (scale ? scale[m] : 1.0) * load(g, c->g_dtype, i);
+        store(u[j], c->m_dtype, i, beta[j] * load(u[j], c->m_dtype, i) + (1.0 - beta[j]) * gh);
+      }
+      if (mask & (1u << (j + 1))) {
+        double acc = 0.0;
+        for (int64_t m = 0; m < K; ++m) acc += load(u[j], c->m_dtype, m * P + p);
+        for (int64_t m = 0; m < K; ++m) store(u[j], c->m_dtype, m * P + p, acc / (double)K);
+      }
+    }
+    for (int64_t m = 0; m < K; ++m) {
+      const int64_t i = m * P + p;
+      const double gh = (scale ? scale[m] : 1.0) * load(g, c->g_dtype, i);
+      double delta = g_weight * gh;
+      for (int32_t j = 0; j < n; ++j) delta += omega[j] * load(u[j], c->m_dtype, i);
+      store(x, c->x_dtype, i, load(x, c->x_dtype, i) - eta * delta);
+    }
+    if (mask & 1u) {
+      double acc = 0.0;
+      for (int64_t m = 0; m < K; ++m) acc += load(x, c->x_dtype, m * P + p);
+      for (int64_t m = 0; m < K; ++m) store(x, c->x_dtype, m * P + p, acc / (double)K);
+    }
+  }
+}
+
 /* --------------------------------------------------------- replica mean */
 
 /* E_m[S]: the arithmetic mean over the K workers of one state, written back

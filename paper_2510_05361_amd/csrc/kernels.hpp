@@ -370,6 +370,112 @@ __global__ __launch_bounds__(kBlock) void k_local_step_sync(StepParams p, uint32
   }
 }
 
+// Probabilistic SGDM variant (Algorithm 4): the first moments due in mask
+// are averaged over the replicas BEFORE the update direction uses them, so
+// every replica steps with the averaged momentum; x is updated and, when
+// bit 0 is set, averaged as in k_local_step_sync.  Two passes per column:
+// pass 1 updates every replica's moments and stores the ones not due (the
+// same thread reloads them in pass 2) and the means of the due ones; pass 2
+// forms each replica's direction and updates x.
+template <int N, typename XT, typename GT, int V, int NTM>
+__global__ __launch_bounds__(kBlock) void k_sgdm_averaged_momenta(StepParams p, uint32_t mask, int32_t K) {
+#pragma clang fp contract(off)
+  constexpr bool NTL = (NTM & 1) != 0, NTS = (NTM & 2) != 0;
+  const bool sync_x = (mask & 1u) != 0;
+  bool sync_u[N];
+#pragma unroll
+  for (int j = 0; j < N; ++j) sync_u[j] = ((mask >> (j + 1)) & 1u) != 0;
+  XT* __restrict__ x = reinterpret_cast<XT*>(p.x);
+  const GT* __restrict__ g = reinterpret_cast<const GT*>(p.g);
+  const float kf = (float)K;
+
+  for (int64_t tile = blockIdx.x; tile < p.tiles; tile += gridDim.x) {
+    const int64_t e = tile * (int64_t)(kBlock * V) + (int64_t)threadIdx.x * V;
+    if (e >= p.P) continue;
+    // pass 1: u^j of every replica; due ones become their replica mean
+    float u0[N][V], du[N][V];
+#pragma unroll
+    for (int j = 0; j < N; ++j)
+#pragma unroll
+      for (int t = 0; t < V; ++t) du[j][t] = 0.0f;
+    for (int32_t m = 0; m < K; ++m) {
+      const int64_t r = (int64_t)m * p.P + e;
+      float gv[V], uv[N][V];
+      load_v<GT, V, NTL>(g, r, gv);
+#pragma unroll
+      for (int j = 0; j < N; ++j) load_v<float, V, NTL>(p.u[j], r, uv[j]);
+      const float sc = p.scale != nullptr ? p.scale[m] : 1.0f;
+#pragma unroll
+      for (int t = 0; t < V; ++t) {
+        const float gh = sc * gv[t];
+#pragma unroll
+        for (int j = 0; j < N; ++j) uv[j][t] = __builtin_fmaf(p.beta[j], uv[j][t], p.omb[j] * gh);
+      }
+#pragma unroll
+      for (int j = 0; j < N; ++j) {
+        if (sync_u[j]) {
+#pragma unroll
+          for (int t = 0; t < V; ++t) {
+            if (m == 0) u0[j][t] = uv[j][t];
+            else du[j][t] += uv[j][t] - u0[j][t];
+          }
+        } else {
+          store_v<float, V, false>(p.u[j], r, uv[j]);
+        }
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < N; ++j) {
+      if (!sync_u[j]) continue;
+#pragma unroll
+      for (int t = 0; t < V; ++t) u0[j][t] = u0[j][t] + du[j][t] / kf;
+      for (int32_t m = 0; m < K; ++m) store_v<float, V, NTS>(p.u[j], (int64_t)m * p.P + e, u0[j]);
+    }
+    // pass 2: direction with the averaged (due) or local (not due) moments
+    float x0[V], dx[V];
+#pragma unroll
+    for (int t = 0; t < V; ++t) dx[t] = 0.0f;
+    for (int32_t m = 0; m < K; ++m) {
+      const int64_t r = (int64_t)m * p.P + e;
+      float gv[V], xv[V], uv[N][V];
+      load_v<GT, V, NTL>(g, r, gv);
+      load_v<XT, V, NTL>(x, r, xv);
+#pragma unroll
+      for (int j = 0; j < N; ++j) {
+        if (sync_u[j]) {
+#pragma unroll
+          for (int t = 0; t < V; ++t) uv[j][t] = u0[j][t];
+        } else {
+          load_v<float, V, false>(p.u[j], r, uv[j]);
+        }
+      }
+      const float sc = p.scale != nullptr ? p.scale[m] : 1.0f;
+#pragma unroll
+      for (int t = 0; t < V; ++t) {
+        const float gh = sc * gv[t];
+        float delta = p.gw * gh;
+#pragma unroll
+        for (int j = 0; j < N; ++j) delta = __builtin_fmaf(p.w[j], uv[j][t], delta);
+        xv[t] = as_stored<XT>(__builtin_fmaf(-p.lr, delta, xv[t]));
+      }
+      if (sync_x) {
+#pragma unroll
+        for (int t = 0; t < V; ++t) {
+          if (m == 0) x0[t] = xv[t];
+          else dx[t] += xv[t] - x0[t];
+        }
+      } else {
+        store_v<XT, V, NTS>(x, r, xv);
+      }
+    }
+    if (sync_x) {
+#pragma unroll
+      for (int t = 0; t < V; ++t) x0[t] = x0[t] + dx[t] / kf;
+      for (int32_t m = 0; m < K; ++m) store_v<XT, V, NTS>(x, (int64_t)m * p.P + e, x0);
+    }
+  }
+}
+
 // ADOPT's first update with the previous-v order: v = g^2, nothing else.
 template <typename GT, int V, int U, bool NT>
 __global__ __launch_bounds__(kBlock) void k_adopt_init_v(const void* gp, float* vp, int64_t P, int64_t tiles) {

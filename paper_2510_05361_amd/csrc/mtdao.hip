@@ -95,6 +95,10 @@ int32_t validate(const mtdao_config* c, std::string* e) {
   if (c->form == MTDAO_ADOPT && c->clip_rho > 0.0f)
     return fail(e, MTDAO_ERR_INVALID_ARG, "ADOPT clips the normalised gradient with c_t (per call), not rho");
   if (c->period_x < 0) return fail(e, MTDAO_ERR_INVALID_ARG, "period_x=%d < 0", c->period_x);
+  if (c->sync_order != MTDAO_SYNC_AFTER_STEP && c->sync_order != MTDAO_SYNC_MOMENTA_IN_STEP)
+    return fail(e, MTDAO_ERR_INVALID_ARG, "sync_order %d is not AFTER_STEP(0) or MOMENTA_IN_STEP(1)", c->sync_order);
+  if (c->sync_order == MTDAO_SYNC_MOMENTA_IN_STEP && c->form != MTDAO_SGDM)
+    return fail(e, MTDAO_ERR_INVALID_ARG, "sync_order MOMENTA_IN_STEP is the SGDM variant (Algorithm 4)");
   if (c->start_step < 0) return fail(e, MTDAO_ERR_INVALID_ARG, "start_step < 0");
   if (c->numel < 0) return fail(e, MTDAO_ERR_INVALID_ARG, "numel < 0");
   if (c->numel > (INT64_C(1) << 40) / c->replicas)
@@ -282,6 +286,21 @@ int launch_blocks(int64_t n) {
   if (b < 1) b = 1;
   if (b > 65536) b = 65536;
   return (int)b;
+}
+
+// Algorithm 4: averaged first moments feed the same step (SGDM only).
+void launch_sgdm_averaged_momenta(const mtdao_config& c, StepParams p, int V, uint32_t mask, hipStream_t st) {
+  dispatch_step(c, V, [&](auto form, auto n, auto xt, auto gt, auto vw) {
+    constexpr int FORM = decltype(form)::value, N = decltype(n)::value, VV = decltype(vw)::value;
+    if constexpr (FORM == kSgdm) {
+      using XT = typename decltype(xt)::type;
+      using GT = typename decltype(gt)::type;
+      const int64_t per = (int64_t)kBlock * VV;
+      p.tiles = (p.P + per - 1) / per;
+      hipLaunchKernelGGL((k_sgdm_averaged_momenta<N, XT, GT, VV, kStepNT>), grid_for(p.tiles, 1), dim3(kBlock), 0, st,
+                         p, mask, c.replicas);
+    }
+  });
 }
 
 }  // namespace
@@ -518,8 +537,11 @@ int32_t mtdao_sync(mtdao_handle* h, uint32_t mask, uint32_t* applied_mask, void*
   uint32_t m;
   int32_t r = resolve_mask(h, mask, h->s, &m);
   if (r != MTDAO_OK) return r;
-  if (applied_mask) *applied_mask = m;
   const mtdao_config& c = h->cfg;
+  if (c.sync_order == MTDAO_SYNC_MOMENTA_IN_STEP && (m & ~1u) != 0)
+    return fail(&h->err, MTDAO_ERR_INVALID_ARG,
+                "with sync_order MOMENTA_IN_STEP the moments are averaged inside mtdao_step_sync (mask 0x%x)", m);
+  if (applied_mask) *applied_mask = m;
   if (m == 0 || c.numel == 0 || c.replicas == 1) return MTDAO_OK;  // K = 1: the mean is the row
   launch_means(h, m, reinterpret_cast<hipStream_t>(hip_stream));
   return hip_check(&h->err, hipGetLastError(), "mtdao_sync launch");
@@ -545,6 +567,8 @@ int32_t mtdao_step_sync(mtdao_handle* h, const void* grads, float lr, float adop
     if (m != 0 && c.replicas > 1) launch_means(h, m, st);
   } else if (m == 0 || c.replicas == 1) {
     launch_step(c, p, step_vec_width(c), st);
+  } else if (c.sync_order == MTDAO_SYNC_MOMENTA_IN_STEP && (m & ~1u) != 0) {
+    launch_sgdm_averaged_momenta(c, p, step_vec_width(c), m, st);
   } else {
     launch_step_sync(c, p, step_vec_width(c), m, st);
   }

@@ -24,6 +24,7 @@ MTDAO_SYNC_AUTO = 0xFFFFFFFF
 MTDAO_ADAM, MTDAO_ADOPT, MTDAO_SGDM = 0, 1, 2
 MTDAO_F32, MTDAO_BF16 = 0, 1
 MTDAO_ADOPT_PREV, MTDAO_ADOPT_CUR = 0, 1
+MTDAO_SYNC_AFTER_STEP, MTDAO_SYNC_MOMENTA_IN_STEP = 0, 1
 MTDAO_OK = 0
 MTDAO_ERR_INVALID_ARG = -1
 MTDAO_ERR_ALIGN = -2
@@ -52,6 +53,7 @@ class MtdaoConfig(ctypes.Structure):
         ("period_x", ctypes.c_int32), ("period_u", ctypes.c_int32 * MTDAO_MAX_N),
         ("period_v", ctypes.c_int32), ("start_step", ctypes.c_int64), ("numel", ctypes.c_int64),
         ("n_tensors", ctypes.c_int32), ("tensor_numel", ctypes.POINTER(ctypes.c_int64)),
+        ("sync_order", ctypes.c_int32),
     ]
 
 
@@ -107,7 +109,7 @@ def make_config(form: str, replicas: int, beta1: Sequence[float], omega: Sequenc
                 param_dtype: str = "f32", grad_dtype: str = "f32", adopt_order: str = "prev",
                 bias_correction: bool = True, period_x: int = 0,
                 period_u: Sequence[int] = (0,), period_v: int = 0, start_step: int = 0,
-                tensor_numel: Optional[Sequence[int]] = None) -> MtdaoConfig:
+                tensor_numel: Optional[Sequence[int]] = None, sync_order: int = 0) -> MtdaoConfig:
     """Fill an ``mtdao_config``.  The returned structure keeps a reference to
     its tensor-size array (``_tensor_arr``) for as long as it lives."""
     n = len(beta1)
@@ -130,6 +132,7 @@ def make_config(form: str, replicas: int, beta1: Sequence[float], omega: Sequenc
     c.period_v = int(period_v)
     c.start_step = int(start_step)
     c.numel = int(numel)
+    c.sync_order = int(sync_order)
     if tensor_numel is not None and len(tensor_numel) > 0:
         arr = (ctypes.c_int64 * len(tensor_numel))(*[int(t) for t in tensor_numel])
         c.n_tensors = len(tensor_numel)
@@ -142,14 +145,14 @@ def make_config(form: str, replicas: int, beta1: Sequence[float], omega: Sequenc
 
 
 def config_from_workload(w, start_step: int = 0, numel: Optional[int] = None,
-                         tensor_numel: Optional[Sequence[int]] = None) -> MtdaoConfig:
+                         tensor_numel: Optional[Sequence[int]] = None, sync_order: int = 0) -> MtdaoConfig:
     """``mtdao_config`` of a ``synth.Workload``."""
     tn = [t.numel for t in w.tensors] if tensor_numel is None and numel is None else tensor_numel
     return make_config(w.form, w.replicas, w.beta1, w.omega, w.numel if numel is None else numel,
                        beta2=w.beta2, eps=w.eps, clip_rho=w.clip_rho, param_dtype=w.param_dtype,
                        grad_dtype=w.grad_dtype, adopt_order=w.adopt_order, bias_correction=True,
                        period_x=w.period_x, period_u=w.period_u, period_v=w.period_v,
-                       start_step=start_step, tensor_numel=tn)
+                       start_step=start_step, tensor_numel=tn, sync_order=sync_order)
 
 
 def mtdao_workspace_bytes(cfg: MtdaoConfig) -> int:

@@ -336,3 +336,18 @@ def sample_indices(w: Workload, n_stride: int = 1 << 16, edge: int = 64) -> np.n
     parts.append(np.arange(0, P, stride, dtype=np.int64)[:n_stride])
     parts.append(np.array([P - 1]))
     return np.unique(np.concatenate(parts).astype(np.int64))
+
+
+def bernoulli_masks(seed: int, steps: int, n_moments: int, p_x: float, p_u: Sequence[float],
+                    p_v: float = 0.0, has_v: bool = False) -> list:
+    """Seeded averaging events of the probabilistic variant (Algorithm 4):
+    after every step each state is averaged with its own probability,
+    independently, the same event for all workers.  Returns one mask per
+    step (bit 0 = x, bit j = u^j, bit N+1 = v)."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    probs = [p_x] + list(p_u) + ([p_v] if has_v else [])
+    out = []
+    for _ in range(steps):
+        draws = rng.random(len(probs))
+        out.append(int(sum(1 << b for b, (d, p) in enumerate(zip(draws, probs)) if d < p)))
+    return out

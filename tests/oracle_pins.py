@@ -431,6 +431,69 @@ def pin_all_periods_one_keeps_workers_identical():
                 assert np.all(a == a[0]), (form, s)
 
 
+def pin_model_only_equals_momenta_only():
+    """Section 3, for the probabilistic variant (Algorithm 4, where an
+    averaged momentum feeds the same step's direction): averaging only the
+    model at every step (p_x = 1, p_j = 0) is algorithmically the same as
+    averaging only the momenta at every step (p_x = 0, p_j = 1): from a
+    common x_0 both keep every worker on the same x, which follows DDP-SGDM
+    on the mean gradient."""
+    rng = np.random.default_rng(28)
+    P, K, T = 13, 4, 20
+    betas, omegas = (0.0, f32(0.9)), (f32(0.3), f32(0.7))
+    x0 = rng.normal(0, 1, P)
+    G = {s: rng.normal(0, 1, (K, P)) for s in range(1, T + 1)}
+    cfg = _cfg("sgdm", betas, omegas, period_x=0, period_u=(0, 0), period_v=0)
+    a, b = oracle.new_state(cfg, x0, K), oracle.new_state(cfg, x0, K)
+    oracle.run_probabilistic(cfg, a, lambda s: G[s], range(1, T + 1), lambda s: f32(0.05), lambda s: 0b001)
+    oracle.run_probabilistic(cfg, b, lambda s: G[s], range(1, T + 1), lambda s: f32(0.05), lambda s: 0b110)
+    x, u = x0.copy(), [np.zeros(P), np.zeros(P)]
+    for s in range(1, T + 1):
+        gm = G[s].mean(axis=0)
+        u = [bj * uj + (1 - bj) * gm for bj, uj in zip(betas, u)]
+        x = x - f32(0.05) * sum(w * uj for w, uj in zip(omegas, u))
+    for m in range(K):
+        _close(a.x[m], x, 1e-12, 1e-14, "model-only")
+        _close(b.x[m], x, 1e-12, 1e-14, "momenta-only")
+    # the deterministic order (Algorithm 3: the local momentum feeds the
+    # step, the average is the next base) does not have this property
+    c = oracle.new_state(cfg, x0, K)
+    oracle.run(cfg, c, lambda s: G[s], range(1, T + 1), lambda s: f32(0.05), masks=lambda s: 0b110)
+    assert np.abs(c.x - c.x[0]).max() > 1e-3
+
+
+def pin_probabilistic_sync_virtual_average():
+    """Algorithm 4 with drawn events (probabilities p_x, p_j; sum of omega =
+    1; the gradient as a beta = 0 momentum): for any event sequence the
+    worker mean of x follows DDP-SGDM on the mean gradient; with no events
+    it is Algorithm 3 without averaging."""
+    import synth
+
+    rng = np.random.default_rng(29)
+    P, K, T = 11, 3, 40
+    betas, omegas = (0.0, f32(0.95)), (f32(0.25), f32(0.75))
+    cfg = _cfg("sgdm", betas, omegas, period_x=0, period_u=(0, 0), period_v=0)
+    masks = synth.bernoulli_masks(7, T, 2, 1 / 4, (1 / 2, 1 / 8))
+    assert any(m & 1 for m in masks) and any(m & 6 for m in masks) and 0 in masks
+    x0 = rng.normal(0, 1, P)
+    G = {s: rng.normal(0, 1, (K, P)) for s in range(1, T + 1)}
+    st = oracle.new_state(cfg, x0, K)
+    applied = oracle.run_probabilistic(cfg, st, lambda s: G[s], range(1, T + 1), lambda s: f32(0.02),
+                                       lambda s: masks[s - 1])
+    assert applied == masks
+    x, u = x0.copy(), [np.zeros(P), np.zeros(P)]
+    for s in range(1, T + 1):
+        gm = G[s].mean(axis=0)
+        u = [b * uj + (1 - b) * gm for b, uj in zip(betas, u)]
+        x = x - f32(0.02) * sum(w * uj for w, uj in zip(omegas, u))
+    _close(st.x.mean(axis=0), x, 1e-12, 1e-14, "mean x")
+    a, b = oracle.new_state(cfg, x0, K), oracle.new_state(cfg, x0, K)
+    oracle.run_probabilistic(cfg, a, lambda s: G[s], range(1, T + 1), lambda s: f32(0.02), lambda s: 0)
+    oracle.run(cfg, b, lambda s: G[s], range(1, T + 1), lambda s: f32(0.02))
+    for p_, q_ in zip(a.arrays(), b.arrays()):
+        assert np.array_equal(p_, q_)
+
+
 # ----------------------------------------------------------------- P9, P11 (paper numbers)
 
 

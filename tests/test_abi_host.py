@@ -64,7 +64,7 @@ BAD = [
     dict(period_x=-1), dict(period_u=(4, -2)), dict(period_v=-3), dict(start_step=-1),
     dict(numel=-5), dict(form="adopt", clip_rho=1.0), dict(clip_rho=float("nan")),
     dict(tensor_numel=[1000, 23]), dict(tensor_numel=[1024, -1, 1]),
-    dict(numel=1 << 39, replicas=8),
+    dict(numel=1 << 39, replicas=8), dict(sync_order=2), dict(sync_order=1), dict(form="adopt", sync_order=1),
 ]
 
 
@@ -191,6 +191,29 @@ def test_handle_host_paths():
         abi.mtdao_destroy(h)
     abi.mtdao_destroy(None)
     assert abi.mtdao_step_count(None) == -1
+
+
+def test_averaged_momenta_order_host_rules():
+    """Algorithm 4's order: moment averaging only inside mtdao_step_sync."""
+    cfg = good_cfg(form="sgdm", sync_order=abi.MTDAO_SYNC_MOMENTA_IN_STEP)
+    h = _fake_handle(cfg)
+    try:
+        for mask in (0b010, 0b100, 0b111):
+            with pytest.raises(abi.MtdaoError) as e:
+                abi.mtdao_sync(h, mask, None)
+            assert e.value.code == abi.MTDAO_ERR_INVALID_ARG
+            assert "inside mtdao_step_sync" in abi.mtdao_last_error(h)
+    finally:
+        abi.mtdao_destroy(h)
+    # numel = 0: the x bit passes validation and launches nothing
+    cfg0 = abi.make_config("sgdm", 3, (0.0, 0.9), (0.3, 0.7), 0, period_x=2, period_u=(4, 4),
+                           sync_order=abi.MTDAO_SYNC_MOMENTA_IN_STEP)
+    h = abi.mtdao_init(cfg0, abi.make_buffers(None, [None] * 2, None, False), None, 0, None)
+    try:
+        assert abi.mtdao_sync(h, 0b001, None) == 0b001
+        assert abi.mtdao_step_sync(h, None, 1e-3, 0.0, 0b111, None) == 0b111
+    finally:
+        abi.mtdao_destroy(h)
 
 
 def test_empty_problem_counts_steps_and_reports_masks():

@@ -369,3 +369,64 @@ def test_step_sync_full_size_bench_workload():
     opt.close()
     del x, u, v, grads
     torch.cuda.empty_cache()
+
+
+# ------------------------------------------------------------ probabilistic variant (Algorithm 4)
+
+
+def _run_prob_gpu(w, steps, masks, dev=None):
+    d = torch.device("cuda:0")
+    dev = dev or DeviceInputs(w, d)
+    cfg = abi.config_from_workload(w, sync_order=abi.MTDAO_SYNC_MOMENTA_IN_STEP)
+    opt = MtdaoOptimizer(cfg, d, x0=dev.x0_row())
+    grads = torch.empty((w.replicas, w.numel), dtype=torch.float32, device=d)
+    applied = []
+    for s, m in zip(steps, masks):
+        dev.grads_into(s, grads)
+        applied.append(opt.step_sync(grads, w.lr, 0.0, m))
+    torch.cuda.synchronize()
+    return opt, applied
+
+
+def _prob_workload(name, **kw):
+    w = synth.WORKLOADS["sgdm_n2_k16_p354m_clip"]
+    # Algorithm 4: sum of omega = 1, the gradient entering as a beta = 0 momentum
+    w = w.replace(beta1=(0.0, 0.99), omega=(0.3, 0.7), clip_rho=0.0, period_x=0, period_u=(0, 0), **kw)
+    return w if name == "full" else synth.small_variant(w, 60_000, tail=37 if name == "odd" else 40)
+
+
+@pytest.mark.parametrize("size", ["aligned", "odd", "full"])
+def test_probabilistic_sync_against_oracle(size):
+    """Bernoulli averaging events (p_x = 1/16, p_u = 1/4, 1/32; drawn on the
+    host) through mtdao_step_sync with the averaged-momenta order, against
+    the oracle's Algorithm 4 on the same events."""
+    w = _prob_workload(size, steps=40 if size == "full" else 64)
+    masks = synth.bernoulli_masks(123, w.steps, 2, 1 / 16, (1 / 4, 1 / 32))
+    assert any(m & 0b010 for m in masks) and any(m & 1 for m in masks)
+    log(f"case prob {size} P={w.numel} K={w.replicas} masks={sum(1 for m in masks if m)}")
+    opt, applied = _run_prob_gpu(w, _steps(w), masks)
+    assert applied == masks
+    idx = synth.sample_indices(w) if size == "full" else None
+    ocfg = oracle.OracleConfig.from_workload(w)
+    ost = oracle.new_state(ocfg, synth.host_x0_row(w, idx), w.replicas)
+    oracle.run_probabilistic(ocfg, ost, lambda s: synth.host_grad_rows(w, s, idx), _steps(w),
+                             lambda s: w.lr, lambda s: masks[s - 1])
+    from gpu_harness import OracleResult
+    compare(w, opt, OracleResult(ost, masks, idx), f"prob-{size}")
+    opt.close()
+    torch.cuda.empty_cache()
+
+
+def test_probabilistic_order_x_only_equals_standard_order():
+    """With only x events the two orders coincide bit for bit; with every
+    moment averaged at every step all replicas stay identical."""
+    w = _prob_workload("aligned", steps=20, replicas=5)
+    masks = [1 if s % 3 == 0 else 0 for s in _steps(w)]
+    a, _ = _run_prob_gpu(w, _steps(w), masks)
+    b, _ = _run_fused(w, _steps(w), masks=masks)
+    for p, q in zip(a.states(), b.states()):
+        assert torch.equal(p, q)
+    c, _ = _run_prob_gpu(w, _steps(w), [0b110] * w.steps)
+    assert torch.equal(c.x, c.x[0:1].expand_as(c.x))
+    for o in (a, b, c):
+        o.close()

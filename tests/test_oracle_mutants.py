@@ -63,6 +63,16 @@ MUTANTS = [
     ("bf16_truncates", "ldexp(nearbyint(ldexp(a, -q)), q)", "ldexp(trunc(ldexp(a, -q)), q)", 0),
     ("bf16_ties_away", "ldexp(nearbyint(ldexp(a, -q)), q)", "ldexp(round(ldexp(a, -q)), q)", 0),
     ("bf16_no_subnormals", "if (q < -133) q = -133;", "if (q < -126) q = -126;", 0),
+    ("prob_step_omega_index", "for (int32_t j = 0; j < n; ++j) delta += omega[j] * load(u[j], c->m_dtype, i);",
+     "for (int32_t j = 0; j < n; ++j) delta += omega[0] * load(u[j], c->m_dtype, i);", 0),
+    ("prob_step_ema_weights_swapped",
+     "store(u[j], c->m_dtype, i, beta[j] * load(u[j], c->m_dtype, i) + (1.0 - beta[j]) * gh);",
+     "store(u[j], c->m_dtype, i, (1.0 - beta[j]) * load(u[j], c->m_dtype, i) + beta[j] * gh);", 0),
+    ("prob_step_u_mean_skips_last_worker",
+     "for (int64_t m = 0; m < K; ++m) acc += load(u[j], c->m_dtype, m * P + p);",
+     "for (int64_t m = 0; m + 1 < K; ++m) acc += load(u[j], c->m_dtype, m * P + p);", 0),
+    ("prob_step_no_x_average", "    if (mask & 1u) {\n      double acc = 0.0;",
+     "    if (mask & 0u) {\n      double acc = 0.0;", 0),
     ("f32_store_truncates", "float f = (float)a;\n    ((float*)p)[i] = f;",
      "float f = (float)a;\n    if ((double)f > a && f > 0) f = nextafterf(f, 0.0f);\n    ((float*)p)[i] = f;", 0),
 ]
