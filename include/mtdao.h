@@ -86,6 +86,21 @@ enum { MTDAO_ADOPT_PREV = 0, MTDAO_ADOPT_CUR = 1 };
  *                              mtdao_step_sync; mtdao_sync then accepts only
  *                              the x bit. */
 enum { MTDAO_SYNC_AFTER_STEP = 0, MTDAO_SYNC_MOMENTA_IN_STEP = 1 };
+/* OuterOpt at an averaging event of x (the Require blocks' OuterOpt,
+ * averaging by default):
+ *   MTDAO_OUTER_AVERAGE   every worker restarts from the mean E_m[x^m]
+ *   MTDAO_OUTER_NESTEROV  outer Nesterov step on the outer parameters xo
+ *                         (fp32 [P]) with outer momentum b (fp32 [P]):
+ *                         d = xo - E_m[x^m]; b = mu b + d;
+ *                         xo = xo - outer_lr (d + mu b); every worker
+ *                         restarts from xo.  outer_lr = 1, mu = 0 is
+ *                         averaging.  Needs sync_order AFTER_STEP. */
+enum { MTDAO_OUTER_AVERAGE = 0, MTDAO_OUTER_NESTEROV = 1 };
+/* State ids of mtdao_read_state beyond the per-worker states
+ * (0 = x, 1..N = u^j, N+1 = v): the outer parameters and momentum of the
+ * Nesterov OuterOpt (fp32, one row: replica must be 0). */
+#define MTDAO_STATE_X_OUTER 6
+#define MTDAO_STATE_OUTER_MOM 7
 /* status codes */
 enum {
   MTDAO_OK = 0,
@@ -121,6 +136,9 @@ typedef struct mtdao_config {
   int32_t n_tensors;        /* entries of tensor_numel (0: one tensor of P elements) */
   const int64_t* tensor_numel; /* host array, sums to P; copied by mtdao_init        */
   int32_t sync_order;       /* MTDAO_SYNC_AFTER_STEP (default) / _MOMENTA_IN_STEP    */
+  int32_t outer_opt;        /* MTDAO_OUTER_AVERAGE (default) / MTDAO_OUTER_NESTEROV  */
+  float outer_lr;           /* Nesterov: outer learning rate > 0                     */
+  float outer_momentum;     /* Nesterov: outer momentum mu in [0,1)                  */
 } mtdao_config;
 
 /* Device state buffers (caller-owned, [K][P] each, see layout above). */
@@ -128,8 +146,11 @@ typedef struct mtdao_buffers {
   void* x;                  /* params                                                */
   float* u[MTDAO_MAX_N];    /* first moments u^1..u^N (entries >= N ignored)         */
   float* v;                 /* second moment (NULL for SGDM)                         */
-  int32_t init_states;      /* 0: x row 0 is broadcast to all rows, u and v zeroed   */
-                            /* 1: all rows of x, u, v are kept as given (resume)     */
+  int32_t init_states;      /* 0: x row 0 is broadcast to all rows, u and v zeroed,  */
+                            /*    x_outer = x row 0 (fp32), x_outer_mom = 0          */
+                            /* 1: all given states are kept as they are (resume)     */
+  float* x_outer;           /* Nesterov OuterOpt: outer parameters, fp32 [P]         */
+  float* x_outer_mom;       /* Nesterov OuterOpt: outer momentum, fp32 [P]           */
 } mtdao_buffers;
 
 typedef struct mtdao_handle mtdao_handle;
@@ -187,8 +208,9 @@ int32_t mtdao_step_sync(mtdao_handle* h, const void* grads, float lr, float adop
 int32_t mtdao_schedule(const mtdao_config* cfg, int64_t s, uint32_t* mask);
 
 /* Copy count elements of one state row to host memory and wait for it:
- *   state    0 = x (cfg.param_dtype), 1..N = u^j, N+1 = v (fp32)
- *   replica  0..K-1;  offset, count within [0, P]
+ *   state    0 = x (cfg.param_dtype), 1..N = u^j, N+1 = v (fp32),
+ *            MTDAO_STATE_X_OUTER / MTDAO_STATE_OUTER_MOM (fp32, Nesterov)
+ *   replica  0..K-1 (0 for the outer states);  offset, count within [0, P]
  *   host_dst caller-owned, count * element-size bytes
  * Enqueued on hip_stream after earlier work; returns when the copy is done. */
 int32_t mtdao_read_state(mtdao_handle* h, int32_t state, int32_t replica, int64_t offset,

@@ -85,6 +85,9 @@ def lib():
                                         ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                                         ctypes.c_int64, ctypes.c_int64]
         L.oracle_replica_mean.restype = None
+        L.oracle_outer_nesterov.restype = None
+        L.oracle_outer_nesterov.argtypes = [ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p,
+                                            ctypes.c_float, ctypes.c_float, ctypes.c_int64, ctypes.c_int64]
         L.oracle_sgdm_prob_step.restype = None
         L.oracle_sgdm_prob_step.argtypes = [ctypes.POINTER(_Cfg), ctypes.c_float, ctypes.c_uint32,
                                             ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
@@ -115,6 +118,9 @@ class OracleConfig:
     period_x: int = 1
     period_u: Sequence[int] = (1,)
     period_v: int = 1
+    outer: str = "average"          # OuterOpt at x events: "average" | "nesterov"
+    outer_lr: float = 1.0
+    outer_momentum: float = 0.0
 
     @property
     def n(self) -> int:
@@ -141,11 +147,13 @@ class OracleConfig:
         return c
 
     @classmethod
-    def from_workload(cls, w, m_dtype: str = "f32") -> "OracleConfig":
+    def from_workload(cls, w, m_dtype: str = "f32", outer: str = "average", outer_lr: float = 1.0,
+                      outer_momentum: float = 0.0) -> "OracleConfig":
         return cls(form=w.form, beta1=tuple(w.beta1), omega=tuple(w.omega), beta2=w.beta2,
                    eps=w.eps, clip_rho=w.clip_rho, bias_correction=True, adopt_order=w.adopt_order,
                    x_dtype=w.param_dtype, g_dtype=w.grad_dtype, m_dtype=m_dtype,
-                   period_x=w.period_x, period_u=tuple(w.period_u), period_v=w.period_v)
+                   period_x=w.period_x, period_u=tuple(w.period_u), period_v=w.period_v,
+                   outer=outer, outer_lr=outer_lr, outer_momentum=outer_momentum)
 
 
 def _ptr(a: np.ndarray) -> int:
@@ -179,15 +187,20 @@ def clip_scales(cfg: OracleConfig, g: np.ndarray) -> Optional[np.ndarray]:
 
 @dataclass
 class OracleState:
-    """All per-worker states, [K][P] arrays in their storage types."""
+    """All per-worker states, [K][P] arrays in their storage types; with a
+    Nesterov OuterOpt also the outer parameters and momentum (fp32 [P])."""
 
     x: np.ndarray
     u: List[np.ndarray]
     v: Optional[np.ndarray]
+    x_outer: Optional[np.ndarray] = None
+    outer_mom: Optional[np.ndarray] = None
 
     def copy(self) -> "OracleState":
         return OracleState(self.x.copy(), [a.copy() for a in self.u],
-                           None if self.v is None else self.v.copy())
+                           None if self.v is None else self.v.copy(),
+                           None if self.x_outer is None else self.x_outer.copy(),
+                           None if self.outer_mom is None else self.outer_mom.copy())
 
     def arrays(self) -> List[np.ndarray]:
         return [self.x] + list(self.u) + ([self.v] if self.v is not None else [])
@@ -202,7 +215,14 @@ def new_state(cfg: OracleConfig, x0_row: np.ndarray, K: int) -> OracleState:
     x = np.repeat(np.asarray(x0_row, dtype=xd).reshape(1, P), K, axis=0)  # always a fresh copy
     u = [np.zeros((K, P), dtype=md) for _ in range(cfg.n)]
     v = np.zeros((K, P), dtype=md) if cfg.has_v else None
-    return OracleState(x, u, v)
+    st = OracleState(x, u, v)
+    if cfg.outer == "nesterov":
+        xf = np.asarray(x0_row)
+        if cfg.x_dtype == "bf16":
+            xf = (xf.astype(np.uint32) << np.uint32(16)).view(np.float32)
+        st.x_outer = np.array(xf, dtype=np.float32).reshape(P)
+        st.outer_mom = np.zeros(P, dtype=np.float32)
+    return st
 
 
 def local_step(cfg: OracleConfig, st: OracleState, g: np.ndarray, s: int, lr: float,
@@ -259,11 +279,22 @@ def replica_mean(a: np.ndarray, dtype: str) -> None:
     lib().oracle_replica_mean(_ptr(a), _DTYPES[dtype], K, P)
 
 
+def outer_nesterov(cfg: OracleConfig, st: OracleState) -> None:
+    """Nesterov OuterOpt at an averaging event of x (in place)."""
+    K, P = st.x.shape
+    assert st.x_outer is not None and st.outer_mom is not None
+    lib().oracle_outer_nesterov(_ptr(st.x), _DTYPES[cfg.x_dtype], _ptr(st.x_outer), _ptr(st.outer_mom),
+                                float(cfg.outer_lr), float(cfg.outer_momentum), K, P)
+
+
 def sync(cfg: OracleConfig, st: OracleState, mask: int) -> None:
     """Average every state whose bit is set in ``mask`` (bit 0 = x, bit j =
     u^j, bit N+1 = v)."""
     if mask & 1:
-        replica_mean(st.x, cfg.x_dtype)
+        if cfg.outer == "nesterov":
+            outer_nesterov(cfg, st)
+        else:
+            replica_mean(st.x, cfg.x_dtype)
     for j in range(cfg.n):
         if mask & (1 << (j + 1)):
             replica_mean(st.u[j], cfg.m_dtype)

@@ -305,5 +305,34 @@ void oracle_replica_mean(void* state, int32_t dtype, int64_t K, int64_t P) {
   }
 }
 
+/* -------------------------------------------------- Nesterov OuterOpt */
+
+/*
+ * OuterOpt = Nesterov momentum at an averaging event of x (the outer
+ * optimizer the paper compares against; the outer Nesterov step of the
+ * local-update literature): with the workers' mean xbar = E_m[x^m], the
+ * outer parameters xo and the outer momentum b (fp32 [P] each),
+ *   d  = xo - xbar            (outer pseudo-gradient)
+ *   b  = mu * b + d
+ *   xo = xo - outer_lr * (d + mu * b)
+ * and every worker restarts from xo.  outer_lr = 1, mu = 0 gives xo = xbar,
+ * plain averaging.
+ */
+void oracle_outer_nesterov(void* x, int32_t x_dtype, float* xo, float* b, float outer_lr, float mu, int64_t K,
+                           int64_t P) {
+  const double lr = (double)outer_lr, m_ = (double)mu;
+  for (int64_t p = 0; p < P; ++p) {
+    double acc = 0.0;
+    for (int64_t m = 0; m < K; ++m) acc += load(x, x_dtype, m * P + p);
+    const double xbar = acc / (double)K;
+    const double d = (double)xo[p] - xbar;
+    const double bn = m_ * (double)b[p] + d;
+    b[p] = (float)bn;
+    const double xn = (double)xo[p] - lr * (d + m_ * (double)b[p]);
+    xo[p] = (float)xn;
+    for (int64_t m = 0; m < K; ++m) store(x, x_dtype, m * P + p, (double)xo[p]);
+  }
+}
+
 /* Size in bytes of one element of a storage type (for the Python side). */
 int64_t oracle_dtype_size(int32_t dtype) { return dtype_size(dtype); }

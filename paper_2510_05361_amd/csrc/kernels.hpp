@@ -123,6 +123,37 @@ __device__ __forceinline__ void store_v(T* __restrict__ p, int64_t e, const floa
   }
 }
 
+// ------------------------------------------------------------ OuterOpt
+
+// Nesterov OuterOpt at an averaging event of x (xo == nullptr: plain
+// averaging).  xo, mom: fp32 [P] outer parameters and outer momentum.
+struct OuterParams {
+  float* xo;
+  float* mom;
+  float lr;   // outer learning rate
+  float mu;   // outer momentum
+};
+
+// xbar (the workers' mean) becomes the value every worker restarts from:
+// d = xo - xbar; mom = mu mom + d; xo = xo - lr (d + mu mom).
+template <int V>
+__device__ __forceinline__ void outer_step(const OuterParams& o, int64_t e, float (&xbar)[V]) {
+#pragma clang fp contract(off)
+  if (o.xo == nullptr) return;
+  float xo[V], b[V];
+  load_v<float, V, false>(o.xo, e, xo);
+  load_v<float, V, false>(o.mom, e, b);
+#pragma unroll
+  for (int t = 0; t < V; ++t) {
+    const float d = xo[t] - xbar[t];
+    b[t] = __builtin_fmaf(o.mu, b[t], d);
+    xo[t] = __builtin_fmaf(-o.lr, __builtin_fmaf(o.mu, b[t], d), xo[t]);
+    xbar[t] = xo[t];
+  }
+  store_v<float, V, false>(o.xo, e, xo);
+  store_v<float, V, false>(o.mom, e, b);
+}
+
 // ------------------------------------------------------------ local step
 
 // Per-launch scalars, prepared on the host in double and rounded to fp32.
@@ -143,6 +174,7 @@ struct StepParams {
   float eps;
   float lr;                // eta_t
   float clip;              // ADOPT c_t (<= 0: no clamp)
+  OuterParams outer;       // OuterOpt applied when x is averaged
 };
 
 // The update of one element of one replica (the loop body of Algorithm 1, 2
@@ -351,6 +383,7 @@ __global__ __launch_bounds__(kBlock) void k_local_step_sync(StepParams p, uint32
     if (sync_x) {
 #pragma unroll
       for (int t = 0; t < V; ++t) x0[t] = x0[t] + dx[t] / kf;
+      outer_step<V>(p.outer, e, x0);
       for (int32_t m = 0; m < K; ++m) store_v<XT, V, NTS>(x, (int64_t)m * p.P + e, x0);
     }
 #pragma unroll
@@ -504,6 +537,8 @@ struct MeanParams {
   int64_t P;
   int64_t tiles;
   int32_t K;
+  int32_t outer_state;          // index of x in state[] when OuterOpt applies, else -1
+  OuterParams outer;
 };
 
 // E_m[S] for the state blockIdx.y: every element becomes
@@ -542,6 +577,7 @@ __global__ __launch_bounds__(kBlock) void k_replica_mean(MeanParams p) {
       if (e >= p.P) continue;
 #pragma unroll
       for (int t = 0; t < V; ++t) s0[k][t] = s0[k][t] + d[k][t] / kf;
+      if ((int32_t)blockIdx.y == p.outer_state) outer_step<V>(p.outer, e, s0[k]);
 #pragma unroll 4
       for (int32_t m = 0; m < p.K; ++m) store_v<T, V, NT>(s + (int64_t)m * p.P, e, s0[k]);
     }
@@ -623,6 +659,16 @@ __global__ __launch_bounds__(kBlock) void k_broadcast_row0(T* __restrict__ x, in
   for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < P; i += stride) {
     const T a = x[i];
     for (int32_t m = 1; m < K; ++m) x[(int64_t)m * P + i] = a;
+  }
+}
+
+// xo[i] = x[0][i] widened to fp32 (the outer parameters start at x_0).
+template <typename T>
+__global__ __launch_bounds__(kBlock) void k_row0_to_f32(const T* __restrict__ x, float* __restrict__ xo, int64_t P) {
+  const int64_t stride = (int64_t)gridDim.x * kBlock;
+  for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < P; i += stride) {
+    if constexpr (sizeof(T) == 2) xo[i] = bf16_to_f32(x[i]);
+    else xo[i] = x[i];
   }
 }
 

@@ -23,6 +23,8 @@ struct mtdao_handle {
   void* x = nullptr;
   float* u[MTDAO_MAX_N] = {nullptr, nullptr, nullptr, nullptr};
   float* v = nullptr;
+  float* x_outer = nullptr;         // Nesterov OuterOpt: outer parameters [P]
+  float* x_outer_mom = nullptr;     // Nesterov OuterOpt: outer momentum [P]
   float* scale = nullptr;           // workspace: [K] clip factors
   double* partials = nullptr;       // workspace: [K][norm_blocks]
   int32_t norm_blocks = 0;
@@ -99,6 +101,16 @@ int32_t validate(const mtdao_config* c, std::string* e) {
     return fail(e, MTDAO_ERR_INVALID_ARG, "sync_order %d is not AFTER_STEP(0) or MOMENTA_IN_STEP(1)", c->sync_order);
   if (c->sync_order == MTDAO_SYNC_MOMENTA_IN_STEP && c->form != MTDAO_SGDM)
     return fail(e, MTDAO_ERR_INVALID_ARG, "sync_order MOMENTA_IN_STEP is the SGDM variant (Algorithm 4)");
+  if (c->outer_opt != MTDAO_OUTER_AVERAGE && c->outer_opt != MTDAO_OUTER_NESTEROV)
+    return fail(e, MTDAO_ERR_INVALID_ARG, "outer_opt %d is not AVERAGE(0) or NESTEROV(1)", c->outer_opt);
+  if (c->outer_opt == MTDAO_OUTER_NESTEROV) {
+    if (!(c->outer_lr > 0.0f) || !std::isfinite(c->outer_lr))
+      return fail(e, MTDAO_ERR_INVALID_ARG, "outer_lr=%g must be finite and > 0", c->outer_lr);
+    if (!(c->outer_momentum >= 0.0f && c->outer_momentum < 1.0f))
+      return fail(e, MTDAO_ERR_INVALID_ARG, "outer_momentum=%g outside [0,1)", c->outer_momentum);
+    if (c->sync_order != MTDAO_SYNC_AFTER_STEP)
+      return fail(e, MTDAO_ERR_INVALID_ARG, "the Nesterov OuterOpt needs sync_order AFTER_STEP");
+  }
   if (c->start_step < 0) return fail(e, MTDAO_ERR_INVALID_ARG, "start_step < 0");
   if (c->numel < 0) return fail(e, MTDAO_ERR_INVALID_ARG, "numel < 0");
   if (c->numel > (INT64_C(1) << 40) / c->replicas)
@@ -347,6 +359,12 @@ int32_t mtdao_init(const mtdao_config* cfg, const mtdao_buffers* bufs, void* wor
       if (!bufs->v) return fail(&g_err, MTDAO_ERR_INVALID_ARG, "v is NULL (Adam and ADOPT need it)");
       ranges.push_back({bufs->v, KP * 4});
     }
+    if (c.outer_opt == MTDAO_OUTER_NESTEROV) {
+      if (!bufs->x_outer || !bufs->x_outer_mom)
+        return fail(&g_err, MTDAO_ERR_INVALID_ARG, "x_outer / x_outer_mom are NULL (Nesterov OuterOpt needs them)");
+      ranges.push_back({bufs->x_outer, c.numel * 4});
+      ranges.push_back({bufs->x_outer_mom, c.numel * 4});
+    }
     for (auto& rg : ranges)
       if (!aligned16(rg.first)) return fail(&g_err, MTDAO_ERR_ALIGN, "a state buffer is not 16-byte aligned");
     for (size_t a = 0; a < ranges.size(); ++a)
@@ -372,6 +390,10 @@ int32_t mtdao_init(const mtdao_config* cfg, const mtdao_buffers* bufs, void* wor
   h->x = bufs->x;
   for (int j = 0; j < N; ++j) h->u[j] = bufs->u[j];
   h->v = has_v(c) ? bufs->v : nullptr;
+  if (c.outer_opt == MTDAO_OUTER_NESTEROV) {
+    h->x_outer = bufs->x_outer;
+    h->x_outer_mom = bufs->x_outer_mom;
+  }
   h->s = c.start_step;
   if (need > 0) {
     const size_t scale_bytes = ((size_t)c.replicas * sizeof(float) + 255) / 256 * 256;
@@ -393,6 +415,14 @@ int32_t mtdao_init(const mtdao_config* cfg, const mtdao_buffers* bufs, void* wor
     const int zb = launch_blocks(KP);
     for (int j = 0; j < N; ++j) hipLaunchKernelGGL(k_fill_zero, dim3(zb), dim3(kBlock), 0, st, h->u[j], KP);
     if (h->v) hipLaunchKernelGGL(k_fill_zero, dim3(zb), dim3(kBlock), 0, st, h->v, KP);
+    if (h->x_outer) {
+      if (c.param_dtype == MTDAO_F32)
+        hipLaunchKernelGGL(k_row0_to_f32<float>, dim3(nb), dim3(kBlock), 0, st, (const float*)h->x, h->x_outer, c.numel);
+      else
+        hipLaunchKernelGGL(k_row0_to_f32<uint16_t>, dim3(nb), dim3(kBlock), 0, st, (const uint16_t*)h->x, h->x_outer,
+                           c.numel);
+      hipLaunchKernelGGL(k_fill_zero, dim3(nb), dim3(kBlock), 0, st, h->x_outer_mom, c.numel);
+    }
     r = hip_check(&g_err, hipGetLastError(), "mtdao_init launch");
     if (r != MTDAO_OK) {
       delete h;
@@ -420,6 +450,7 @@ int32_t check_step_args(mtdao_handle* h, const void* grads, float lr, float adop
     bool ov = overlap(grads, gb, h->x, KP * esize(c.param_dtype));
     for (int j = 0; j < c.n_moments; ++j) ov = ov || overlap(grads, gb, h->u[j], KP * 4);
     if (h->v) ov = ov || overlap(grads, gb, h->v, KP * 4);
+    if (h->x_outer) ov = ov || overlap(grads, gb, h->x_outer, P * 4) || overlap(grads, gb, h->x_outer_mom, P * 4);
     if (ov) return fail(&h->err, MTDAO_ERR_INVALID_ARG, "grads overlaps a state buffer");
   }
   return MTDAO_OK;
@@ -436,6 +467,15 @@ int32_t resolve_mask(mtdao_handle* h, uint32_t mask, int64_t s, uint32_t* out) {
                 1 + c.n_moments + (has_v(c) ? 1 : 0));
   *out = mask;
   return MTDAO_OK;
+}
+
+OuterParams outer_params(const mtdao_handle* h) {
+  OuterParams o;
+  o.xo = h->x_outer;
+  o.mom = h->x_outer_mom;
+  o.lr = h->cfg.outer_lr;
+  o.mu = h->cfg.outer_momentum;
+  return o;
 }
 
 // Per-step scalars of update s in double, rounded once to fp32; launches
@@ -467,6 +507,7 @@ StepParams prepare_step(mtdao_handle* h, const void* grads, float lr, float adop
   p.lr = lr;
   p.clip = adopt_clip;
   p.scale = nullptr;
+  p.outer = outer_params(h);
   if (c.form != MTDAO_ADOPT && c.clip_rho > 0.0f) {
     const int Vg = (P % 4 == 0) ? 4 : 1;  // 16-byte (fp32) or 8-byte (bf16) slots
     if (c.grad_dtype == MTDAO_F32) launch_norm<float>(grads, P, c.replicas, Vg, h->norm_blocks, h->partials, st);
@@ -501,9 +542,14 @@ void launch_means(mtdao_handle* h, uint32_t m, hipStream_t st) {
   std::memset(&mp, 0, sizeof mp);
   mp.P = c.numel;
   mp.K = c.replicas;
+  mp.outer_state = -1;
+  mp.outer = outer_params(h);
   // fp32 moment states (and fp32 x) in one launch, bf16 x in its own
   int n = 0;
-  if ((m & 1u) && c.param_dtype == MTDAO_F32) mp.state[n++] = h->x;
+  if ((m & 1u) && c.param_dtype == MTDAO_F32) {
+    if (h->x_outer) mp.outer_state = n;
+    mp.state[n++] = h->x;
+  }
   for (int j = 0; j < c.n_moments; ++j)
     if (m & (1u << (j + 1))) mp.state[n++] = h->u[j];
   if (h->v && (m & (1u << (c.n_moments + 1)))) mp.state[n++] = h->v;
@@ -511,6 +557,7 @@ void launch_means(mtdao_handle* h, uint32_t m, hipStream_t st) {
   if ((m & 1u) && c.param_dtype == MTDAO_BF16) {
     MeanParams xp = mp;
     xp.state[0] = h->x;
+    xp.outer_state = h->x_outer ? 0 : -1;
     launch_mean<uint16_t>(xp, 1, vec_width(MTDAO_BF16, c.numel), st);
   }
 }
@@ -580,10 +627,13 @@ int32_t mtdao_read_state(mtdao_handle* h, int32_t state, int32_t replica, int64_
   if (!h) return fail(&g_err, MTDAO_ERR_INVALID_ARG, "handle is NULL");
   const mtdao_config& c = h->cfg;
   const int32_t nstates = 1 + c.n_moments + (has_v(c) ? 1 : 0);
-  if (state < 0 || state >= nstates)
+  const bool outer_state = state == MTDAO_STATE_X_OUTER || state == MTDAO_STATE_OUTER_MOM;
+  if (outer_state && !h->x_outer)
+    return fail(&h->err, MTDAO_ERR_INVALID_ARG, "state %d needs the Nesterov OuterOpt", state);
+  if (!outer_state && (state < 0 || state >= nstates))
     return fail(&h->err, MTDAO_ERR_INVALID_ARG, "state %d outside [0, %d)", state, nstates);
-  if (replica < 0 || replica >= c.replicas)
-    return fail(&h->err, MTDAO_ERR_RANGE, "replica %d outside [0, %d)", replica, c.replicas);
+  if (replica < 0 || replica >= (outer_state ? 1 : c.replicas))
+    return fail(&h->err, MTDAO_ERR_RANGE, "replica %d outside [0, %d)", replica, outer_state ? 1 : c.replicas);
   if (offset < 0 || count < 0 || offset > c.numel || count > c.numel - offset)
     return fail(&h->err, MTDAO_ERR_RANGE, "range [%lld, +%lld) outside [0, %lld)", (long long)offset,
                 (long long)count, (long long)c.numel);
@@ -591,7 +641,10 @@ int32_t mtdao_read_state(mtdao_handle* h, int32_t state, int32_t replica, int64_
   if (!host_dst) return fail(&h->err, MTDAO_ERR_INVALID_ARG, "host_dst is NULL");
   const void* base;
   int64_t es;
-  if (state == 0) {
+  if (outer_state) {
+    base = state == MTDAO_STATE_X_OUTER ? h->x_outer : h->x_outer_mom;
+    es = 4;
+  } else if (state == 0) {
     base = h->x;
     es = esize(c.param_dtype);
   } else if (state <= c.n_moments) {

@@ -25,6 +25,8 @@ MTDAO_ADAM, MTDAO_ADOPT, MTDAO_SGDM = 0, 1, 2
 MTDAO_F32, MTDAO_BF16 = 0, 1
 MTDAO_ADOPT_PREV, MTDAO_ADOPT_CUR = 0, 1
 MTDAO_SYNC_AFTER_STEP, MTDAO_SYNC_MOMENTA_IN_STEP = 0, 1
+MTDAO_OUTER_AVERAGE, MTDAO_OUTER_NESTEROV = 0, 1
+MTDAO_STATE_X_OUTER, MTDAO_STATE_OUTER_MOM = 6, 7
 MTDAO_OK = 0
 MTDAO_ERR_INVALID_ARG = -1
 MTDAO_ERR_ALIGN = -2
@@ -53,14 +55,15 @@ class MtdaoConfig(ctypes.Structure):
         ("period_x", ctypes.c_int32), ("period_u", ctypes.c_int32 * MTDAO_MAX_N),
         ("period_v", ctypes.c_int32), ("start_step", ctypes.c_int64), ("numel", ctypes.c_int64),
         ("n_tensors", ctypes.c_int32), ("tensor_numel", ctypes.POINTER(ctypes.c_int64)),
-        ("sync_order", ctypes.c_int32),
+        ("sync_order", ctypes.c_int32), ("outer_opt", ctypes.c_int32), ("outer_lr", ctypes.c_float),
+        ("outer_momentum", ctypes.c_float),
     ]
 
 
 class MtdaoBuffers(ctypes.Structure):
     _fields_ = [
         ("x", ctypes.c_void_p), ("u", ctypes.c_void_p * MTDAO_MAX_N), ("v", ctypes.c_void_p),
-        ("init_states", ctypes.c_int32),
+        ("init_states", ctypes.c_int32), ("x_outer", ctypes.c_void_p), ("x_outer_mom", ctypes.c_void_p),
     ]
 
 
@@ -109,7 +112,8 @@ def make_config(form: str, replicas: int, beta1: Sequence[float], omega: Sequenc
                 param_dtype: str = "f32", grad_dtype: str = "f32", adopt_order: str = "prev",
                 bias_correction: bool = True, period_x: int = 0,
                 period_u: Sequence[int] = (0,), period_v: int = 0, start_step: int = 0,
-                tensor_numel: Optional[Sequence[int]] = None, sync_order: int = 0) -> MtdaoConfig:
+                tensor_numel: Optional[Sequence[int]] = None, sync_order: int = 0,
+                outer_opt: int = 0, outer_lr: float = 1.0, outer_momentum: float = 0.0) -> MtdaoConfig:
     """Fill an ``mtdao_config``.  The returned structure keeps a reference to
     its tensor-size array (``_tensor_arr``) for as long as it lives."""
     n = len(beta1)
@@ -133,6 +137,9 @@ def make_config(form: str, replicas: int, beta1: Sequence[float], omega: Sequenc
     c.start_step = int(start_step)
     c.numel = int(numel)
     c.sync_order = int(sync_order)
+    c.outer_opt = int(outer_opt)
+    c.outer_lr = outer_lr
+    c.outer_momentum = outer_momentum
     if tensor_numel is not None and len(tensor_numel) > 0:
         arr = (ctypes.c_int64 * len(tensor_numel))(*[int(t) for t in tensor_numel])
         c.n_tensors = len(tensor_numel)
@@ -145,14 +152,16 @@ def make_config(form: str, replicas: int, beta1: Sequence[float], omega: Sequenc
 
 
 def config_from_workload(w, start_step: int = 0, numel: Optional[int] = None,
-                         tensor_numel: Optional[Sequence[int]] = None, sync_order: int = 0) -> MtdaoConfig:
+                         tensor_numel: Optional[Sequence[int]] = None, sync_order: int = 0,
+                outer_opt: int = 0, outer_lr: float = 1.0, outer_momentum: float = 0.0) -> MtdaoConfig:
     """``mtdao_config`` of a ``synth.Workload``."""
     tn = [t.numel for t in w.tensors] if tensor_numel is None and numel is None else tensor_numel
     return make_config(w.form, w.replicas, w.beta1, w.omega, w.numel if numel is None else numel,
                        beta2=w.beta2, eps=w.eps, clip_rho=w.clip_rho, param_dtype=w.param_dtype,
                        grad_dtype=w.grad_dtype, adopt_order=w.adopt_order, bias_correction=True,
                        period_x=w.period_x, period_u=w.period_u, period_v=w.period_v,
-                       start_step=start_step, tensor_numel=tn, sync_order=sync_order)
+                       start_step=start_step, tensor_numel=tn, sync_order=sync_order, outer_opt=outer_opt,
+                       outer_lr=outer_lr, outer_momentum=outer_momentum)
 
 
 def mtdao_workspace_bytes(cfg: MtdaoConfig) -> int:
@@ -167,9 +176,12 @@ def mtdao_schedule(cfg: MtdaoConfig, s: int) -> int:
     return int(out.value)
 
 
-def make_buffers(x: int, u: Sequence[int], v: Optional[int], init_states: bool) -> MtdaoBuffers:
+def make_buffers(x: int, u: Sequence[int], v: Optional[int], init_states: bool,
+                 x_outer: Optional[int] = None, x_outer_mom: Optional[int] = None) -> MtdaoBuffers:
     b = MtdaoBuffers()
     b.x = x
+    b.x_outer = x_outer
+    b.x_outer_mom = x_outer_mom
     for j, p in enumerate(u):
         b.u[j] = p
     b.v = v

@@ -30,7 +30,8 @@ class MtdaoOptimizer:
 
     def __init__(self, cfg: abi.MtdaoConfig, device: torch.device, x0: Optional[torch.Tensor] = None,
                  resume: bool = False, x: Optional[torch.Tensor] = None,
-                 u: Optional[List[torch.Tensor]] = None, v: Optional[torch.Tensor] = None):
+                 u: Optional[List[torch.Tensor]] = None, v: Optional[torch.Tensor] = None,
+                 x_outer: Optional[torch.Tensor] = None, x_outer_mom: Optional[torch.Tensor] = None):
         self.cfg = cfg
         K, P, N = cfg.replicas, cfg.numel, cfg.n_moments
         self.K, self.P, self.N = K, P, N
@@ -46,10 +47,20 @@ class MtdaoOptimizer:
                 self.x[0].copy_(x0.to(device=device, dtype=xdt))
             self.u = [torch.empty((K, P), dtype=torch.float32, device=device) for _ in range(N)]
             self.v = torch.empty((K, P), dtype=torch.float32, device=device) if self.has_v else None
+        self.x_outer = self.x_outer_mom = None
+        if cfg.outer_opt == abi.MTDAO_OUTER_NESTEROV:
+            if resume:
+                assert x_outer is not None and x_outer_mom is not None
+                self.x_outer, self.x_outer_mom = x_outer, x_outer_mom
+            else:
+                self.x_outer = torch.empty(P, dtype=torch.float32, device=device)
+                self.x_outer_mom = torch.empty(P, dtype=torch.float32, device=device)
         ws = abi.mtdao_workspace_bytes(cfg)
         self.workspace = torch.empty(max(ws, 1), dtype=torch.uint8, device=device)
         bufs = abi.make_buffers(self.x.data_ptr(), [a.data_ptr() for a in self.u],
-                                self.v.data_ptr() if self.v is not None else None, resume)
+                                self.v.data_ptr() if self.v is not None else None, resume,
+                                self.x_outer.data_ptr() if self.x_outer is not None else None,
+                                self.x_outer_mom.data_ptr() if self.x_outer_mom is not None else None)
         self.handle = abi.mtdao_init(cfg, bufs, self.workspace.data_ptr(), self.workspace.numel(), _stream())
 
     # state id 0 = x, 1..N = u^j, N+1 = v

@@ -494,6 +494,60 @@ def pin_probabilistic_sync_virtual_average():
         assert np.array_equal(p_, q_)
 
 
+def pin_outer_nesterov_unit_lr_no_momentum_is_averaging():
+    """OuterOpt = Nesterov with outer_lr = 1, mu = 0 is the default
+    averaging: the outer parameters become the worker mean."""
+    rng = np.random.default_rng(30)
+    P, K, T = 17, 3, 24
+    kw = dict(beta2=f32(0.99), eps=f32(1e-8), period_x=4, period_u=(3, 0), period_v=5)
+    a_cfg = _cfg("adam", (f32(0.9), f32(0.99)), (f32(0.3), f32(0.5)), **kw)
+    b_cfg = _cfg("adam", (f32(0.9), f32(0.99)), (f32(0.3), f32(0.5)), outer="nesterov", outer_lr=1.0,
+                 outer_momentum=0.0, **kw)
+    x0 = rng.normal(0, 1, P)
+    G = {s: rng.normal(0, 1, (K, P)) for s in range(1, T + 1)}
+    a, b = oracle.new_state(a_cfg, x0, K), oracle.new_state(b_cfg, x0, K)
+    oracle.run(a_cfg, a, lambda s: G[s], range(1, T + 1), lambda s: f32(1e-2))
+    oracle.run(b_cfg, b, lambda s: G[s], range(1, T + 1), lambda s: f32(1e-2))
+    # the outer parameters are kept in fp32: agreement to fp32 rounding
+    _close(b.x, a.x, 3e-7, 1e-12, "nesterov(1, 0) vs averaging")
+    _close(b.x_outer, b.x[0], 0, 0, "workers restart from the outer parameters")
+    assert np.all(b.outer_mom == 0) or np.max(np.abs(b.outer_mom)) < 1.0
+
+
+def pin_outer_nesterov_is_torch_sgd_nesterov():
+    """At every averaging event of x the outer parameters take one step of
+    torch.optim.SGD(lr, momentum, nesterov=True) on the outer gradient
+    x_outer - mean_m(x^m), and every worker restarts from them."""
+    rng = np.random.default_rng(31)
+    P, K, T = 20, 3, 36
+    lr_out, mu = f32(0.7), f32(0.9)
+    cfg = _cfg("sgdm", (f32(0.9),), (f32(0.8),), period_x=4, period_u=(6,), period_v=0,
+               outer="nesterov", outer_lr=lr_out, outer_momentum=mu)
+    x0 = rng.normal(0, 1, P).astype(np.float32).astype(np.float64)  # fp32 outer copy holds x0 exactly
+    st = oracle.new_state(cfg, x0, K)
+    p = torch.tensor(x0, dtype=torch.float64, requires_grad=True)
+    opt = torch.optim.SGD([p], lr=lr_out, momentum=mu, nesterov=True)
+    events = 0
+    for s in range(1, T + 1):
+        g = rng.normal(0, 1, (K, P))
+        oracle.local_step(cfg, st, g, s, f32(0.05))
+        mask = oracle.schedule(cfg, s)
+        if mask & 1:
+            mean = st.x.astype(np.float64).mean(axis=0)
+            p.grad = p.detach() - torch.tensor(mean, dtype=torch.float64)
+            opt.step()
+            events += 1
+        oracle.sync(cfg, st, mask)
+        if mask & 1:
+            _close(st.x_outer, p.detach().numpy(), 2e-6, 1e-9, f"outer params s={s}")
+            _close(st.outer_mom, opt.state[p]["momentum_buffer"].numpy(), 2e-6, 1e-9, f"outer mom s={s}")
+            for m in range(K):
+                _close(st.x[m], st.x_outer, 0, 0, "restart")
+            p.data = torch.tensor(st.x_outer.astype(np.float64))  # follow the fp32 outer copy
+            opt.state[p]["momentum_buffer"] = torch.tensor(st.outer_mom.astype(np.float64))
+    assert events == T // 4
+
+
 # ----------------------------------------------------------------- P9, P11 (paper numbers)
 
 

@@ -35,7 +35,8 @@ def test_library_exports_every_declared_symbol():
 
 def test_header_enums_match_binding():
     text = open(HEADER).read()
-    for name in ["MTDAO_ADAM", "MTDAO_ADOPT", "MTDAO_SGDM", "MTDAO_F32", "MTDAO_BF16", "MTDAO_OK",
+    for name in ["MTDAO_OUTER_AVERAGE", "MTDAO_OUTER_NESTEROV", "MTDAO_SYNC_AFTER_STEP", "MTDAO_SYNC_MOMENTA_IN_STEP",
+                 "MTDAO_ADAM", "MTDAO_ADOPT", "MTDAO_SGDM", "MTDAO_F32", "MTDAO_BF16", "MTDAO_OK",
                  "MTDAO_ERR_INVALID_ARG", "MTDAO_ERR_ALIGN", "MTDAO_ERR_HIP", "MTDAO_ERR_RANGE",
                  "MTDAO_ERR_WORKSPACE", "MTDAO_ADOPT_PREV", "MTDAO_ADOPT_CUR"]:
         m = re.search(rf"\b{name}\s*=\s*(-?\d+)", text)
@@ -65,6 +66,9 @@ BAD = [
     dict(numel=-5), dict(form="adopt", clip_rho=1.0), dict(clip_rho=float("nan")),
     dict(tensor_numel=[1000, 23]), dict(tensor_numel=[1024, -1, 1]),
     dict(numel=1 << 39, replicas=8), dict(sync_order=2), dict(sync_order=1), dict(form="adopt", sync_order=1),
+    dict(outer_opt=2), dict(outer_opt=1, outer_lr=0.0), dict(outer_opt=1, outer_lr=float("inf")),
+    dict(outer_opt=1, outer_momentum=1.0), dict(outer_opt=1, outer_momentum=-0.1),
+    dict(form="sgdm", outer_opt=1, sync_order=1),
 ]
 
 
@@ -191,6 +195,41 @@ def test_handle_host_paths():
         abi.mtdao_destroy(h)
     abi.mtdao_destroy(None)
     assert abi.mtdao_step_count(None) == -1
+
+
+def test_outer_nesterov_host_rules():
+    cfg = good_cfg(outer_opt=abi.MTDAO_OUTER_NESTEROV, outer_lr=0.7, outer_momentum=0.9)
+    abi.mtdao_workspace_bytes(cfg)
+    bufs = abi.make_buffers(1 << 40, [1 << 41, 1 << 42], 1 << 43, True)  # outer buffers missing
+    with pytest.raises(abi.MtdaoError) as e:
+        abi.mtdao_init(cfg, bufs, None, 0, None)
+    assert e.value.code == abi.MTDAO_ERR_INVALID_ARG and "x_outer" in abi.mtdao_last_error(None)
+    bufs = abi.make_buffers(1 << 40, [1 << 41, 1 << 42], 1 << 43, True, 1 << 44, (1 << 44) + 64)
+    with pytest.raises(abi.MtdaoError) as e:  # outer buffers overlap each other
+        abi.mtdao_init(cfg, bufs, None, 0, None)
+    assert e.value.code == abi.MTDAO_ERR_INVALID_ARG
+    bufs = abi.make_buffers(1 << 40, [1 << 41, 1 << 42], 1 << 43, True, 1 << 44, (1 << 44) + 8)
+    with pytest.raises(abi.MtdaoError) as e:
+        abi.mtdao_init(cfg, bufs, None, 0, None)
+    bufs = abi.make_buffers(1 << 40, [1 << 41, 1 << 42], 1 << 43, True, 1 << 44, 1 << 45)
+    h = abi.mtdao_init(cfg, bufs, None, 0, None)
+    try:
+        dst = np.zeros(4, dtype=np.float32)
+        with pytest.raises(abi.MtdaoError) as e:
+            abi.mtdao_read_state(h, abi.MTDAO_STATE_X_OUTER, 1, 0, 4, dst, None)
+        assert e.value.code == abi.MTDAO_ERR_RANGE
+        with pytest.raises(abi.MtdaoError) as e:
+            abi.mtdao_local_step(h, (1 << 44) + 128, 1e-3, 0.0, None)  # overlaps x_outer
+        assert e.value.code == abi.MTDAO_ERR_INVALID_ARG
+    finally:
+        abi.mtdao_destroy(h)
+    h = _fake_handle(good_cfg())
+    try:
+        with pytest.raises(abi.MtdaoError) as e:
+            abi.mtdao_read_state(h, abi.MTDAO_STATE_X_OUTER, 0, 0, 4, np.zeros(4, np.float32), None)
+        assert e.value.code == abi.MTDAO_ERR_INVALID_ARG
+    finally:
+        abi.mtdao_destroy(h)
 
 
 def test_averaged_momenta_order_host_rules():

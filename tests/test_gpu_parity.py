@@ -430,3 +430,84 @@ def test_probabilistic_order_x_only_equals_standard_order():
     assert torch.equal(c.x, c.x[0:1].expand_as(c.x))
     for o in (a, b, c):
         o.close()
+
+
+# ------------------------------------------------------------ Nesterov OuterOpt
+
+NESTEROV = (0.7, 0.9)
+
+
+@pytest.mark.parametrize("name", ["adam_n3_k4_p16m", "adopt_n2_k8_p124m_bf16", "sgdm_n2_k16_p354m_clip"])
+@pytest.mark.parametrize("fused", [False, True], ids=["separate", "fused"])
+def test_outer_nesterov_against_oracle(name, fused):
+    """Nesterov OuterOpt at every averaging event of x, through the separate
+    and the fused entry points, against the oracle (x, moments, outer
+    parameters and outer momentum)."""
+    w = synth.small_variant(synth.WORKLOADS[name], 40_000, tail=8)
+    w = w.replace(steps=min(w.steps, 96), period_x=max(2, w.period_x // 8))
+    log(f"case nesterov {w.name} fused={fused} period_x={w.period_x}")
+    g = run_gpu(w, _steps(w), outer=NESTEROV, fused=fused)
+    o = run_oracle(w, _steps(w), outer=NESTEROV)
+    assert g.masks == o.masks and sum(m & 1 for m in g.masks) >= 4
+    compare(w, g.opt, o, f"nesterov-{name}-{fused}")
+    assert torch.equal(g.opt.x, g.opt.x[0:1].expand_as(g.opt.x)) or (g.masks[-1] & 1) == 0
+    free(g)
+
+
+def test_outer_nesterov_fused_bit_identical_and_resume():
+    w = synth.small_variant(synth.WORKLOADS["adam_n3_k4_p16m"], 40_000, tail=8).replace(
+        steps=70, period_x=8)
+    d = torch.device("cuda:0")
+    dev = DeviceInputs(w, d)
+    a = run_gpu(w, _steps(w), outer=NESTEROV, dev=dev)
+    b = run_gpu(w, _steps(w), outer=NESTEROV, dev=dev, fused=True)
+    assert a.masks == b.masks
+    for p, q in zip(a.opt.states() + [a.opt.x_outer, a.opt.x_outer_mom],
+                    b.opt.states() + [b.opt.x_outer, b.opt.x_outer_mom]):
+        assert torch.equal(p, q)
+    # resume: read the outer states through mtdao_read_state, restart at s = 40
+    cut = 40
+    c = run_gpu(w, list(range(1, cut + 1)), outer=NESTEROV, dev=dev)
+    st = torch.cuda.current_stream().cuda_stream
+    xo = np.empty(w.numel, dtype=np.float32)
+    xm = np.empty(w.numel, dtype=np.float32)
+    abi.mtdao_read_state(c.opt.handle, abi.MTDAO_STATE_X_OUTER, 0, 0, w.numel, xo, st)
+    abi.mtdao_read_state(c.opt.handle, abi.MTDAO_STATE_OUTER_MOM, 0, 0, w.numel, xm, st)
+    assert np.array_equal(xo, c.opt.x_outer.cpu().numpy()) and np.array_equal(xm, c.opt.x_outer_mom.cpu().numpy())
+    with pytest.raises(abi.MtdaoError):
+        abi.mtdao_read_state(c.opt.handle, abi.MTDAO_STATE_X_OUTER, 1, 0, 4, xo, st)
+    from gpu_harness import gpu_config
+    opt = MtdaoOptimizer(gpu_config(w, cut, NESTEROV), d, resume=True, x=c.opt.x.clone(),
+                         u=[t.clone() for t in c.opt.u], v=c.opt.v.clone(),
+                         x_outer=torch.from_numpy(xo).to(d), x_outer_mom=torch.from_numpy(xm).to(d))
+    r = run_gpu(w, list(range(cut + 1, w.steps + 1)), dev=dev, opt=opt)
+    for p, q in zip(a.opt.states() + [a.opt.x_outer, a.opt.x_outer_mom],
+                    r.opt.states() + [r.opt.x_outer, r.opt.x_outer_mom]):
+        assert torch.equal(p, q)
+    free(a, b, c, r)
+
+
+def test_outer_nesterov_unit_lr_is_averaging():
+    """outer_lr = 1, momentum 0 restarts every worker from the mean."""
+    w = synth.small_variant(synth.WORKLOADS["sgdm_n2_k16_p354m_clip"], 30_000).replace(steps=48)
+    a = run_gpu(w, _steps(w))
+    b = run_gpu(w, _steps(w), outer=(1.0, 0.0))
+    from gpu_harness import rel_err
+    for p, q in zip(a.opt.states(), b.opt.states()):
+        assert rel_err(q.cpu().numpy(), p.cpu().numpy()) < 1e-6
+    free(a, b)
+
+
+def test_outer_nesterov_full_size_bench_workload():
+    """The 1.31B-parameter K=4 workload with the Nesterov OuterOpt through
+    the fused entry point over 128 steps (x averaged at 64 and 128),
+    sampled against the oracle."""
+    w = synth.WORKLOADS["adam_n3_k4_p1311m"].replace(steps=128)
+    idx = synth.sample_indices(w)
+    g = run_gpu(w, _steps(w), outer=NESTEROV, fused=True)
+    o = run_oracle(w, _steps(w), idx, outer=NESTEROV)
+    assert g.masks == o.masks
+    from gpu_harness import OracleResult
+    # the outer rows are [P]; compare them on the sample too
+    compare(w, g.opt, OracleResult(o.state, o.masks, idx), "nesterov-full")
+    free(g)

@@ -73,6 +73,9 @@ MUTANTS = [
      "for (int64_t m = 0; m + 1 < K; ++m) acc += load(u[j], c->m_dtype, m * P + p);", 0),
     ("prob_step_no_x_average", "    if (mask & 1u) {\n      double acc = 0.0;",
      "    if (mask & 0u) {\n      double acc = 0.0;", 0),
+    ("outer_plain_momentum", "(double)xo[p] - lr * (d + m_ * (double)b[p]);", "(double)xo[p] - lr * ((double)b[p]);", 0),
+    ("outer_gradient_sign", "const double d = (double)xo[p] - xbar;", "const double d = xbar - (double)xo[p];", 0),
+    ("outer_no_momentum", "const double bn = m_ * (double)b[p] + d;", "const double bn = d;", 0),
     ("f32_store_truncates", "float f = (float)a;\n    ((float*)p)[i] = f;",
      "float f = (float)a;\n    if ((double)f > a && f > 0) f = nextafterf(f, 0.0f);\n    ((float*)p)[i] = f;", 0),
 ]
