@@ -241,7 +241,10 @@ def compare(w: synth.Workload, gpu: MtdaoOptimizer, orc: OracleResult, label: st
                          rel_err=rel_err(synth.bf16_bits_to_f32(a), synth.bf16_bits_to_f32(o)))
             report[name] = stats
             log(f"  {label} {name}: {stats}")
-            assert stats["max_ulps"] <= BF16_MAX_ULPS, (label, name, stats)
+            # with a Nesterov OuterOpt every worker restarts from the outer
+            # parameters, which carry flips amplified by lr (1 + mu) / (1 - mu)
+            max_ulps = BF16_OUTER_MAX_ULPS if gpu.x_outer is not None else BF16_MAX_ULPS
+            assert stats["max_ulps"] <= max_ulps, (label, name, stats)
             assert stats["frac_gt1"] <= BF16_FRAC_GT1, (label, name, stats)
             assert stats["frac_ge1"] <= BF16_FRAC_GE1, (label, name, stats)
         else:
