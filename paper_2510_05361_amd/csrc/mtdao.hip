@@ -36,7 +36,9 @@ namespace {
 
 thread_local std::string g_err;
 
-constexpr int kStepU = 2;      // vector slots per thread in the local step
+// Vector slots per thread in the local step (measured on MI355X: two for
+// Adam's 6-read/5-write stream, one for SGDM and ADOPT).
+constexpr int step_slots(int form) { return form == kAdam ? 2 : 1; }
 constexpr int kStepNT = 3;     // nontemporal hints of the local step (bit 0 loads, bit 1 stores)
 constexpr bool kMeanNT = true; // nontemporal hints of the replica mean
 constexpr int kNormU = 4;      // vector slots per thread in the norm pass
@@ -184,17 +186,15 @@ struct TypeC {
 };
 
 // Calls f(form, n, xtype, gtype, vwidth) with compile-time constants for the
-// configuration of c and the runtime vector width V (1, or 4 for fp32-only
-// rows, 8 when a bf16 buffer is involved).
+// configuration of c and the runtime vector width V (4, or 1 when a row
+// length breaks the 4-element alignment of row starts).
 template <typename F>
 void dispatch_step(const mtdao_config& c, int V, F&& f) {
   auto with_types = [&](auto form, auto n) {
     auto with_v = [&](auto xt, auto gt) {
-      using XT = typename decltype(xt)::type;
-      using GT = typename decltype(gt)::type;
-      constexpr int VW = (sizeof(XT) == 2 || sizeof(GT) == 2) ? 8 : 4;
+      // 4-element slots: 16-byte fp32 and 8-byte bf16 accesses per lane
       if (V == 1) f(form, n, xt, gt, IntC<1>{});
-      else f(form, n, xt, gt, IntC<VW>{});
+      else f(form, n, xt, gt, IntC<4>{});
     };
     if (c.param_dtype == MTDAO_F32 && c.grad_dtype == MTDAO_F32) with_v(TypeC<float>{}, TypeC<float>{});
     else if (c.param_dtype == MTDAO_F32) with_v(TypeC<float>{}, TypeC<uint16_t>{});
@@ -220,16 +220,17 @@ void launch_step(const mtdao_config& c, StepParams p, int V, hipStream_t st) {
     constexpr int FORM = decltype(form)::value, N = decltype(n)::value, VV = decltype(vw)::value;
     using XT = typename decltype(xt)::type;
     using GT = typename decltype(gt)::type;
-    const int64_t per = (int64_t)kBlock * VV * kStepU;
+    constexpr int U = step_slots(FORM);
+    const int64_t per = (int64_t)kBlock * VV * U;
     p.tiles = (p.P + per - 1) / per;
     const dim3 grid = grid_for(p.tiles, c.replicas);
     if constexpr (FORM == kAdopt) {
       if (c.adopt_order == MTDAO_ADOPT_CUR) {
-        hipLaunchKernelGGL((k_local_step<FORM, N, XT, GT, VV, kStepU, kStepNT, kCur>), grid, dim3(kBlock), 0, st, p);
+        hipLaunchKernelGGL((k_local_step<FORM, N, XT, GT, VV, U, kStepNT, kCur>), grid, dim3(kBlock), 0, st, p);
         return;
       }
     }
-    hipLaunchKernelGGL((k_local_step<FORM, N, XT, GT, VV, kStepU, kStepNT, kPrev>), grid, dim3(kBlock), 0, st, p);
+    hipLaunchKernelGGL((k_local_step<FORM, N, XT, GT, VV, U, kStepNT, kPrev>), grid, dim3(kBlock), 0, st, p);
   });
 }
 
@@ -257,12 +258,12 @@ void launch_step_sync(const mtdao_config& c, StepParams p, int V, uint32_t mask,
 
 template <typename GT>
 void launch_adopt_init(const void* g, float* v, int64_t P, int32_t K, int V, hipStream_t st) {
-  const int64_t per = (int64_t)kBlock * kStepU;
+  const int64_t per = (int64_t)kBlock * 2;
   if (V == 1) {
-    hipLaunchKernelGGL((k_adopt_init_v<GT, 1, kStepU, false>), grid_for((P + per - 1) / per, K), dim3(kBlock), 0, st,
+    hipLaunchKernelGGL((k_adopt_init_v<GT, 1, 2, false>), grid_for((P + per - 1) / per, K), dim3(kBlock), 0, st,
                        g, v, P, (P + per - 1) / per);
   } else {
-    hipLaunchKernelGGL((k_adopt_init_v<GT, 4, kStepU, false>), grid_for((P + 4 * per - 1) / (4 * per), K), dim3(kBlock),
+    hipLaunchKernelGGL((k_adopt_init_v<GT, 4, 2, false>), grid_for((P + 4 * per - 1) / (4 * per), K), dim3(kBlock),
                        0, st, g, v, P, (P + 4 * per - 1) / (4 * per));
   }
 }
@@ -519,11 +520,9 @@ StepParams prepare_step(mtdao_handle* h, const void* grads, float lr, float adop
   return p;
 }
 
-// One vector width for every buffer the step touches.
-int step_vec_width(const mtdao_config& c) {
-  return (c.param_dtype == MTDAO_BF16 || c.grad_dtype == MTDAO_BF16) ? vec_width(MTDAO_BF16, c.numel)
-                                                                       : vec_width(MTDAO_F32, c.numel);
-}
+// One vector width for every buffer the step touches: 4 elements when every
+// row start keeps 16-byte (fp32) and 8-byte (bf16) alignment, else 1.
+int step_vec_width(const mtdao_config& c) { return (c.numel % 4 == 0) ? 4 : 1; }
 
 bool adopt_first_update(const mtdao_config& c, int64_t s) {
   return c.form == MTDAO_ADOPT && c.adopt_order == MTDAO_ADOPT_PREV && s == 1;

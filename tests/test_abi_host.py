@@ -325,3 +325,40 @@ def test_bf16_input_conversion():
     b = synth.bf16_bits_to_f32(synth.f32_to_bf16_bits(a))
     t = torch.from_numpy(a).to(torch.bfloat16).float().numpy()
     assert np.array_equal(b[:5], t[:5]) and np.isnan(b[5])
+
+
+def test_binding_struct_layout_matches_header(tmp_path):
+    """Every field of mtdao_config and mtdao_buffers sits at the same offset
+    with the same size in the ctypes binding as in the C header (a stale
+    mirror would hand the library garbage pointers)."""
+    import ctypes
+    import os
+    import subprocess
+
+    structs = {"mtdao_config": abi.MtdaoConfig, "mtdao_buffers": abi.MtdaoBuffers}
+    lines = ["#include <stdio.h>", "#include <stddef.h>", '#include "mtdao.h"', "int main(void) {"]
+    for cname, py in structs.items():
+        lines.append(f'  printf("{cname} sizeof %zu\\n", sizeof({cname}));')
+        for fname, _ in py._fields_:
+            lines.append(f'  printf("{cname} {fname} %zu %zu\\n", offsetof({cname}, {fname}), '
+                         f'sizeof((({cname}*)0)->{fname}));')
+    lines.append("  return 0; }")
+    src = tmp_path / "layout.c"
+    src.write_text("\n".join(lines))
+    exe = tmp_path / "layout"
+    inc = os.path.join(os.path.dirname(HEADER))
+    subprocess.run(["gcc", "-std=c11", "-I", inc, "-o", str(exe), str(src)], check=True)
+    out = subprocess.run([str(exe)], check=True, capture_output=True, text=True).stdout.split("\n")
+    seen = 0
+    for line in out:
+        if not line:
+            continue
+        parts = line.split()
+        py = structs[parts[0]]
+        if parts[1] == "sizeof":
+            assert int(parts[2]) == ctypes.sizeof(py), line
+        else:
+            fld = getattr(py, parts[1])
+            assert (fld.offset, fld.size) == (int(parts[2]), int(parts[3])), line
+            seen += 1
+    assert seen == sum(len(p._fields_) for p in structs.values())
