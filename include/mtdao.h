@@ -101,6 +101,27 @@ enum { MTDAO_OUTER_AVERAGE = 0, MTDAO_OUTER_NESTEROV = 1 };
  * Nesterov OuterOpt (fp32, one row: replica must be 0). */
 #define MTDAO_STATE_X_OUTER 6
 #define MTDAO_STATE_OUTER_MOM 7
+
+/* Averaging diagnostics (mtdao_sync_stats), per averaged state, from its
+ * values before averaging, over all P elements (Section 4.1, other
+ * metrics).  The vectors are c^m = S^m, or, for x under the Nesterov
+ * OuterOpt, the pseudo-gradients c^m = x_outer - x^m; cbar is their mean:
+ *   [MTDAO_STAT_MEAN_SQ]      ||cbar||^2
+ *   [MTDAO_STAT_VARIANCE]     (1/K) sum_m ||c^m - cbar||^2  (cross-worker variance)
+ *   [MTDAO_STAT_OUTER_SQ]     ||x_outer||^2 before the outer step (x under
+ *                             Nesterov; 0 otherwise); the relative change
+ *                             of the model over the round is
+ *                             sqrt(MEAN_SQ / OUTER_SQ)
+ *   [MTDAO_STAT_WORKER_SQ + m]  ||c^m||^2
+ *   [MTDAO_STAT_WORKER_DOT + m] <c^m, cbar>   (cosine = DOT / sqrt(SQ * MEAN_SQ))
+ * Workers m < K; K <= MTDAO_STATS_MAX_REPLICAS. */
+#define MTDAO_STATS_MAX_REPLICAS 16
+#define MTDAO_STATS_STRIDE 36
+#define MTDAO_STAT_MEAN_SQ 0
+#define MTDAO_STAT_VARIANCE 1
+#define MTDAO_STAT_OUTER_SQ 2
+#define MTDAO_STAT_WORKER_SQ 4
+#define MTDAO_STAT_WORKER_DOT 20
 /* status codes */
 enum {
   MTDAO_OK = 0,
@@ -202,6 +223,22 @@ int32_t mtdao_sync(mtdao_handle* h, uint32_t mask, uint32_t* applied_mask, void*
  * not move when an argument is rejected. */
 int32_t mtdao_step_sync(mtdao_handle* h, const void* grads, float lr, float adopt_clip, uint32_t mask,
                         uint32_t* applied_mask, void* hip_stream);
+
+/* Device scratch (bytes) that mtdao_sync_stats needs for this
+ * configuration (per-block partial sums of the diagnostics).  Host-only. */
+int32_t mtdao_stats_scratch_bytes(const mtdao_config* cfg, size_t* bytes);
+
+/* mtdao_sync(mask) that also returns the averaging diagnostics of every
+ * averaged state, computed in the same pass from the values before they are
+ * averaged (the averaged values are bit-identical to mtdao_sync's).
+ *   scratch     device buffer of mtdao_stats_scratch_bytes, 256-byte aligned,
+ *               caller-owned (contents are scratch between calls)
+ *   host_stats  caller-owned host array of (MTDAO_MAX_N + 2) *
+ *               MTDAO_STATS_STRIDE doubles, indexed [state id][stat]; the
+ *               rows of states not averaged are NaN
+ * Needs K <= MTDAO_STATS_MAX_REPLICAS.  Waits for the stream. */
+int32_t mtdao_sync_stats(mtdao_handle* h, uint32_t mask, uint32_t* applied_mask, void* scratch, size_t scratch_bytes,
+                         double* host_stats, void* hip_stream);
 
 /* The schedule alone: states due after update s for this configuration.
  * Host-only; no GPU needed. */

@@ -88,6 +88,9 @@ def lib():
         L.oracle_outer_nesterov.restype = None
         L.oracle_outer_nesterov.argtypes = [ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p,
                                             ctypes.c_float, ctypes.c_float, ctypes.c_int64, ctypes.c_int64]
+        L.oracle_state_stats.restype = None
+        L.oracle_state_stats.argtypes = [ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p, ctypes.c_int64,
+                                         ctypes.c_int64, ctypes.c_void_p]
         L.oracle_sgdm_prob_step.restype = None
         L.oracle_sgdm_prob_step.argtypes = [ctypes.POINTER(_Cfg), ctypes.c_float, ctypes.c_uint32,
                                             ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
@@ -285,6 +288,35 @@ def outer_nesterov(cfg: OracleConfig, st: OracleState) -> None:
     assert st.x_outer is not None and st.outer_mom is not None
     lib().oracle_outer_nesterov(_ptr(st.x), _DTYPES[cfg.x_dtype], _ptr(st.x_outer), _ptr(st.outer_mom),
                                 float(cfg.outer_lr), float(cfg.outer_momentum), K, P)
+
+
+def state_stats(a: np.ndarray, dtype: str, x_outer: Optional[np.ndarray] = None) -> np.ndarray:
+    """Diagnostics of a [K][P] state before it is averaged (see
+    oracle_state_stats): [||cbar||^2, cross-worker variance, ||x_outer||^2, 0,
+    ||c^m||^2 (K), <c^m, cbar> (K)], c^m = S^m or x_outer - x^m."""
+    K, P = a.shape
+    out = np.zeros(4 + 2 * K, dtype=np.float64)
+    xo = None
+    if x_outer is not None:
+        x_outer = np.ascontiguousarray(x_outer, dtype=np.float32)
+        xo = _ptr(x_outer)
+    lib().oracle_state_stats(_ptr(a), _DTYPES[dtype], xo, K, P, _ptr(out))
+    return out
+
+
+def sync_stats(cfg: OracleConfig, st: OracleState, mask: int) -> dict:
+    """Diagnostics of every state in mask from its pre-average values, then
+    the averaging itself.  Returns {state id: stats array}."""
+    out = {}
+    if mask & 1:
+        out[0] = state_stats(st.x, cfg.x_dtype, st.x_outer if cfg.outer == "nesterov" else None)
+    for j in range(cfg.n):
+        if mask & (1 << (j + 1)):
+            out[j + 1] = state_stats(st.u[j], cfg.m_dtype)
+    if st.v is not None and mask & (1 << (cfg.n + 1)):
+        out[cfg.n + 1] = state_stats(st.v, cfg.m_dtype)
+    sync(cfg, st, mask)
+    return out
 
 
 def sync(cfg: OracleConfig, st: OracleState, mask: int) -> None:

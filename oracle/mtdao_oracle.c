@@ -334,5 +334,43 @@ void oracle_outer_nesterov(void* x, int32_t x_dtype, float* xo, float* b, float 
   }
 }
 
+/* ------------------------------------------------ averaging diagnostics */
+
+/*
+ * Diagnostics of one state across the workers (Section 4.1, other
+ * metrics: cross-worker variance, relative change, cosine alignment), from
+ * the values before they are averaged.  With xo == NULL the vectors are the
+ * workers' states c^m = S^m; with the outer parameters xo of a Nesterov
+ * OuterOpt they are the workers' pseudo-gradients c^m = xo - x^m.  cbar is
+ * their mean.  out (4 + 2 K doubles):
+ *   out[0] = ||cbar||^2
+ *   out[1] = (1/K) sum_m ||c^m - cbar||^2      (cross-worker variance)
+ *   out[2] = ||xo||^2 (0 without xo)           (relative change = sqrt(out[0] / out[2]))
+ *   out[3] = 0
+ *   out[4 + m]     = ||c^m||^2
+ *   out[4 + K + m] = <c^m, cbar>               (cosine = out[4+K+m] / sqrt(out[4+m] out[0]))
+ */
+void oracle_state_stats(const void* s, int32_t dtype, const float* xo, int64_t K, int64_t P, double* out) {
+  for (int64_t k = 0; k < 4 + 2 * K; ++k) out[k] = 0.0;
+  for (int64_t p = 0; p < P; ++p) {
+    double cbar = 0.0;
+    for (int64_t m = 0; m < K; ++m) {
+      const double v = load(s, dtype, m * P + p);
+      cbar += xo ? (double)xo[p] - v : v;
+    }
+    cbar /= (double)K;
+    out[0] += cbar * cbar;
+    if (xo) out[2] += (double)xo[p] * (double)xo[p];
+    for (int64_t m = 0; m < K; ++m) {
+      const double v = load(s, dtype, m * P + p);
+      const double c = xo ? (double)xo[p] - v : v;
+      out[1] += (c - cbar) * (c - cbar);
+      out[4 + m] += c * c;
+      out[4 + K + m] += c * cbar;
+    }
+  }
+  out[1] /= (double)K;
+}
+
 /* Size in bytes of one element of a storage type (for the Python side). */
 int64_t oracle_dtype_size(int32_t dtype) { return dtype_size(dtype); }

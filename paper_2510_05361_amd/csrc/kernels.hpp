@@ -650,6 +650,99 @@ __global__ __launch_bounds__(64) void k_clip_finalize(const double* __restrict__
   }
 }
 
+// ------------------------------------------------ averaging diagnostics
+
+constexpr int kStatsMaxK = 16;
+constexpr int kStatsStride = 4 + 2 * kStatsMaxK;  // doubles per state (layout in mtdao.h)
+
+// The replica mean of k_replica_mean (same arithmetic, same order, same
+// results) plus, from the values before averaging, per block partial sums
+// of the averaging diagnostics of state blockIdx.y: ||cbar||^2,
+// sum_m ||c^m - cbar||^2, ||xo||^2, ||c^m||^2 and <c^m, cbar>, with
+// c^m = S^m, or c^m = xo - x^m for x under a Nesterov OuterOpt.  Needs
+// K <= kStatsMaxK (every row of a column is held in registers).
+template <typename T, int V>
+__global__ __launch_bounds__(kBlock) void k_replica_mean_stats(MeanParams p, double* __restrict__ partials) {
+  T* __restrict__ s = reinterpret_cast<T*>(p.state[blockIdx.y]);
+  const bool outer = (int32_t)blockIdx.y == p.outer_state && p.outer.xo != nullptr;
+  const int32_t K = p.K;
+  const float kf = (float)K;
+  double a_mean = 0.0, a_var = 0.0, a_ref = 0.0, a_sq[kStatsMaxK], a_dot[kStatsMaxK];
+#pragma unroll
+  for (int m = 0; m < kStatsMaxK; ++m) a_sq[m] = a_dot[m] = 0.0;
+  for (int64_t tile = blockIdx.x; tile < p.tiles; tile += gridDim.x) {
+    const int64_t e = tile * (int64_t)(kBlock * V) + (int64_t)threadIdx.x * V;
+    if (e >= p.P) continue;
+    float r[kStatsMaxK][V];
+#pragma unroll
+    for (int m = 0; m < kStatsMaxK; ++m)
+      if (m < K) load_v<T, V, true>(s + (int64_t)m * p.P, e, r[m]);
+    float mean[V], xo[V];
+#pragma unroll
+    for (int t = 0; t < V; ++t) {
+      float d = 0.0f;
+#pragma unroll
+      for (int m = 1; m < kStatsMaxK; ++m)
+        if (m < K) d += r[m][t] - r[0][t];
+      mean[t] = r[0][t] + d / kf;
+    }
+    if (outer) load_v<float, V, false>(p.outer.xo, e, xo);
+#pragma unroll
+    for (int t = 0; t < V; ++t) {
+      const double cbar = outer ? (double)xo[t] - (double)mean[t] : (double)mean[t];
+      a_mean += cbar * cbar;
+      if (outer) a_ref += (double)xo[t] * (double)xo[t];
+#pragma unroll
+      for (int m = 0; m < kStatsMaxK; ++m) {
+        if (m >= K) continue;
+        const double c = outer ? (double)xo[t] - (double)r[m][t] : (double)r[m][t];
+        a_var += (c - cbar) * (c - cbar);
+        a_sq[m] += c * c;
+        a_dot[m] += c * cbar;
+      }
+    }
+    if (outer) outer_step<V>(p.outer, e, mean);
+    for (int32_t m = 0; m < K; ++m) store_v<T, V, true>(s + (int64_t)m * p.P, e, mean);
+  }
+  // block reduction of every diagnostic, fixed order
+  __shared__ double red[kBlock / 64][kStatsStride];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  double vals[kStatsStride];
+  vals[0] = a_mean;
+  vals[1] = a_var;
+  vals[2] = a_ref;
+  vals[3] = 0.0;
+#pragma unroll
+  for (int m = 0; m < kStatsMaxK; ++m) {
+    vals[4 + m] = a_sq[m];
+    vals[4 + kStatsMaxK + m] = a_dot[m];
+  }
+#pragma unroll
+  for (int k = 0; k < kStatsStride; ++k) {
+    const double w = wave_sum(vals[k]);
+    if (lane == 0) red[wave][k] = w;
+  }
+  __syncthreads();
+  if (threadIdx.x < kStatsStride) {
+    double t = 0.0;
+#pragma unroll
+    for (int i = 0; i < kBlock / 64; ++i) t += red[i][threadIdx.x];
+    partials[((int64_t)blockIdx.y * gridDim.x + blockIdx.x) * kStatsStride + threadIdx.x] = t;
+  }
+}
+
+// out[state][k] = sum over blocks of partials (fixed order); the variance
+// sum is divided by K.
+__global__ __launch_bounds__(64) void k_stats_finalize(const double* __restrict__ partials, int32_t nb, int32_t K,
+                                                       double* __restrict__ out) {
+  const int32_t state = blockIdx.x;
+  for (int32_t k = threadIdx.x; k < kStatsStride; k += 64) {
+    double t = 0.0;
+    for (int32_t b = 0; b < nb; ++b) t += partials[((int64_t)state * nb + b) * kStatsStride + k];
+    out[(int64_t)state * kStatsStride + k] = (k == 1) ? t / (double)K : t;
+  }
+}
+
 // ------------------------------------------------------------ init
 
 // Rows 1..K-1 of x <- row 0 (every worker starts from the same x_0).

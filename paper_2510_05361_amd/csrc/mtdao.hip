@@ -294,6 +294,22 @@ void launch_mean(MeanParams p, int nstates, int V, hipStream_t st) {
   }
 }
 
+constexpr int kStatsBlocksMax = 1024;
+
+int32_t stats_blocks_for(int64_t P) {
+  int64_t nb = (P + 4 * kBlock - 1) / (4 * kBlock);
+  if (nb < 1) nb = 1;
+  if (nb > kStatsBlocksMax) nb = kStatsBlocksMax;
+  return (int32_t)nb;
+}
+
+size_t stats_scratch_for(const mtdao_config& c) {
+  // partials of up to 2 + N states (fp32 launch) + 1 (bf16 x launch), then the
+  // finalized rows of both launches
+  const size_t states = (size_t)(2 + c.n_moments + 1);
+  return states * kStatsBlocksMax * kStatsStride * sizeof(double) + 2 * (2 + kMaxN) * kStatsStride * sizeof(double);
+}
+
 int launch_blocks(int64_t n) {
   int64_t b = (n + kBlock - 1) / kBlock;
   if (b < 1) b = 1;
@@ -327,6 +343,14 @@ int32_t mtdao_workspace_bytes(const mtdao_config* cfg, size_t* bytes) {
   if (r != MTDAO_OK) return r;
   if (!bytes) return fail(&g_err, MTDAO_ERR_INVALID_ARG, "bytes is NULL");
   *bytes = workspace_for(*cfg);
+  return MTDAO_OK;
+}
+
+int32_t mtdao_stats_scratch_bytes(const mtdao_config* cfg, size_t* bytes) {
+  const int32_t r = validate(cfg, &g_err);
+  if (r != MTDAO_OK) return r;
+  if (!bytes) return fail(&g_err, MTDAO_ERR_INVALID_ARG, "bytes is NULL");
+  *bytes = stats_scratch_for(*cfg);
   return MTDAO_OK;
 }
 
@@ -591,6 +615,91 @@ int32_t mtdao_sync(mtdao_handle* h, uint32_t mask, uint32_t* applied_mask, void*
   if (m == 0 || c.numel == 0 || c.replicas == 1) return MTDAO_OK;  // K = 1: the mean is the row
   launch_means(h, m, reinterpret_cast<hipStream_t>(hip_stream));
   return hip_check(&h->err, hipGetLastError(), "mtdao_sync launch");
+}
+
+int32_t mtdao_sync_stats(mtdao_handle* h, uint32_t mask, uint32_t* applied_mask, void* scratch, size_t scratch_bytes,
+                         double* host_stats, void* hip_stream) {
+  if (!h) return fail(&g_err, MTDAO_ERR_INVALID_ARG, "handle is NULL");
+  const mtdao_config& c = h->cfg;
+  if (c.replicas > kStatsMaxK)
+    return fail(&h->err, MTDAO_ERR_INVALID_ARG, "diagnostics support up to %d replicas (K=%d)", kStatsMaxK, c.replicas);
+  if (!host_stats) return fail(&h->err, MTDAO_ERR_INVALID_ARG, "host_stats is NULL");
+  const size_t need = stats_scratch_for(c);
+  if (!scratch || scratch_bytes < need)
+    return fail(&h->err, MTDAO_ERR_WORKSPACE, "stats scratch of %zu bytes required", need);
+  if ((reinterpret_cast<uintptr_t>(scratch) & 255u) != 0)
+    return fail(&h->err, MTDAO_ERR_ALIGN, "stats scratch is not 256-byte aligned");
+  uint32_t m;
+  int32_t r = resolve_mask(h, mask, h->s, &m);
+  if (r != MTDAO_OK) return r;
+  if (c.sync_order == MTDAO_SYNC_MOMENTA_IN_STEP && (m & ~1u) != 0)
+    return fail(&h->err, MTDAO_ERR_INVALID_ARG,
+                "with sync_order MOMENTA_IN_STEP the moments are averaged inside mtdao_step_sync (mask 0x%x)", m);
+  if (applied_mask) *applied_mask = m;
+  const int nslots = 2 + kMaxN;
+  for (int i = 0; i < nslots * kStatsStride; ++i) host_stats[i] = NAN;
+  if (m == 0 || c.numel == 0) return MTDAO_OK;
+  hipStream_t st = reinterpret_cast<hipStream_t>(hip_stream);
+  double* partials = reinterpret_cast<double*>(scratch);
+  const size_t part_per_state = (size_t)kStatsBlocksMax * kStatsStride;
+  double* out = partials + (size_t)(2 + c.n_moments + 1) * part_per_state;  // [2][nslots][stride]
+  const int32_t nb = stats_blocks_for(c.numel);
+  // state ids of the fp32 launch, in launch order
+  int ids[2 + kMaxN];
+  MeanParams mp;
+  std::memset(&mp, 0, sizeof mp);
+  mp.P = c.numel;
+  mp.K = c.replicas;
+  mp.outer_state = -1;
+  mp.outer = outer_params(h);
+  int n = 0;
+  if ((m & 1u) && c.param_dtype == MTDAO_F32) {
+    if (h->x_outer) mp.outer_state = n;
+    ids[n] = 0;
+    mp.state[n++] = h->x;
+  }
+  for (int j = 0; j < c.n_moments; ++j)
+    if (m & (1u << (j + 1))) {
+      ids[n] = j + 1;
+      mp.state[n++] = h->u[j];
+    }
+  if (h->v && (m & (1u << (c.n_moments + 1)))) {
+    ids[n] = c.n_moments + 1;
+    mp.state[n++] = h->v;
+  }
+  const bool fp32_vec = c.numel % 4 == 0, bf16_vec = c.numel % 4 == 0;  // 16-byte / 8-byte slots
+  if (n > 0) {
+    MeanParams q = mp;
+    q.tiles = fp32_vec ? (c.numel + 4 * kBlock - 1) / (4 * kBlock) : (c.numel + kBlock - 1) / kBlock;
+    if (fp32_vec) hipLaunchKernelGGL((k_replica_mean_stats<float, 4>), dim3(nb, n), dim3(kBlock), 0, st, q, partials);
+    else hipLaunchKernelGGL((k_replica_mean_stats<float, 1>), dim3(nb, n), dim3(kBlock), 0, st, q, partials);
+    hipLaunchKernelGGL(k_stats_finalize, dim3(n), dim3(64), 0, st, partials, nb, c.replicas, out);
+  }
+  const bool bf16_x = (m & 1u) && c.param_dtype == MTDAO_BF16;
+  if (bf16_x) {
+    MeanParams q = mp;
+    std::memset(q.state, 0, sizeof q.state);
+    q.state[0] = h->x;
+    q.outer_state = h->x_outer ? 0 : -1;
+    q.tiles = bf16_vec ? (c.numel + 4 * kBlock - 1) / (4 * kBlock) : (c.numel + kBlock - 1) / kBlock;
+    double* part_x = partials + (size_t)(2 + c.n_moments) * part_per_state;
+    if (bf16_vec) hipLaunchKernelGGL((k_replica_mean_stats<uint16_t, 4>), dim3(nb, 1), dim3(kBlock), 0, st, q, part_x);
+    else hipLaunchKernelGGL((k_replica_mean_stats<uint16_t, 1>), dim3(nb, 1), dim3(kBlock), 0, st, q, part_x);
+    hipLaunchKernelGGL(k_stats_finalize, dim3(1), dim3(64), 0, st, part_x, nb, c.replicas, out + nslots * kStatsStride);
+  }
+  r = hip_check(&h->err, hipGetLastError(), "mtdao_sync_stats launch");
+  if (r != MTDAO_OK) return r;
+  std::vector<double> rows((size_t)2 * nslots * kStatsStride);
+  r = hip_check(&h->err, hipMemcpyAsync(rows.data(), out, rows.size() * sizeof(double), hipMemcpyDeviceToHost, st),
+                "mtdao_sync_stats copy");
+  if (r != MTDAO_OK) return r;
+  r = hip_check(&h->err, hipStreamSynchronize(st), "mtdao_sync_stats wait");
+  if (r != MTDAO_OK) return r;
+  for (int i = 0; i < n; ++i)
+    for (int k = 0; k < kStatsStride; ++k) host_stats[ids[i] * kStatsStride + k] = rows[(size_t)i * kStatsStride + k];
+  if (bf16_x)
+    for (int k = 0; k < kStatsStride; ++k) host_stats[k] = rows[(size_t)nslots * kStatsStride + k];
+  return MTDAO_OK;
 }
 
 int32_t mtdao_step_sync(mtdao_handle* h, const void* grads, float lr, float adopt_clip, uint32_t mask,

@@ -27,6 +27,9 @@ MTDAO_ADOPT_PREV, MTDAO_ADOPT_CUR = 0, 1
 MTDAO_SYNC_AFTER_STEP, MTDAO_SYNC_MOMENTA_IN_STEP = 0, 1
 MTDAO_OUTER_AVERAGE, MTDAO_OUTER_NESTEROV = 0, 1
 MTDAO_STATE_X_OUTER, MTDAO_STATE_OUTER_MOM = 6, 7
+MTDAO_STATS_MAX_REPLICAS, MTDAO_STATS_STRIDE = 16, 36
+MTDAO_STAT_MEAN_SQ, MTDAO_STAT_VARIANCE, MTDAO_STAT_OUTER_SQ = 0, 1, 2
+MTDAO_STAT_WORKER_SQ, MTDAO_STAT_WORKER_DOT = 4, 20
 MTDAO_OK = 0
 MTDAO_ERR_INVALID_ARG = -1
 MTDAO_ERR_ALIGN = -2
@@ -88,6 +91,10 @@ def lib() -> ctypes.CDLL:
         L.mtdao_sync.restype = I32
         L.mtdao_step_sync.argtypes = [VP, VP, ctypes.c_float, ctypes.c_float, U32, P(U32), VP]
         L.mtdao_step_sync.restype = I32
+        L.mtdao_stats_scratch_bytes.argtypes = [P(MtdaoConfig), P(ctypes.c_size_t)]
+        L.mtdao_stats_scratch_bytes.restype = I32
+        L.mtdao_sync_stats.argtypes = [VP, U32, P(U32), VP, ctypes.c_size_t, VP, VP]
+        L.mtdao_sync_stats.restype = I32
         L.mtdao_schedule.argtypes = [P(MtdaoConfig), I64, P(U32)]
         L.mtdao_schedule.restype = I32
         L.mtdao_read_state.argtypes = [VP, I32, I32, I64, I64, VP, VP]
@@ -213,6 +220,22 @@ def mtdao_step_sync(h: int, grads: int, lr: float, adopt_clip: float, mask: int,
     _check(lib().mtdao_step_sync(h, grads, float(lr), float(adopt_clip), int(mask) & 0xFFFFFFFF,
                                  ctypes.byref(applied), stream), h)
     return int(applied.value)
+
+
+def mtdao_stats_scratch_bytes(cfg: MtdaoConfig) -> int:
+    out = ctypes.c_size_t(0)
+    _check(lib().mtdao_stats_scratch_bytes(ctypes.byref(cfg), ctypes.byref(out)))
+    return int(out.value)
+
+
+def mtdao_sync_stats(h: int, mask: int, scratch: Optional[int], scratch_bytes: int,
+                     stream: Optional[int]):
+    """Returns (applied mask, stats array [MTDAO_MAX_N + 2][MTDAO_STATS_STRIDE])."""
+    applied = ctypes.c_uint32(0)
+    out = np.empty((MTDAO_MAX_N + 2, MTDAO_STATS_STRIDE), dtype=np.float64)
+    _check(lib().mtdao_sync_stats(h, int(mask) & 0xFFFFFFFF, ctypes.byref(applied), scratch, int(scratch_bytes),
+                                  out.ctypes.data, stream), h)
+    return int(applied.value), out
 
 
 def mtdao_read_state(h: int, state: int, replica: int, offset: int, count: int,

@@ -81,6 +81,16 @@ class MtdaoOptimizer:
     def sync(self, mask: int = abi.MTDAO_SYNC_AUTO) -> int:
         return abi.mtdao_sync(self.handle, mask, _stream())
 
+    def sync_stats(self, mask: int = abi.MTDAO_SYNC_AUTO):
+        """mtdao_sync with the averaging diagnostics of every averaged state;
+        returns (applied mask, [state id][stat] array, NaN rows for states not
+        averaged).  The scratch buffer is allocated on first use."""
+        if getattr(self, "_stats_scratch", None) is None:
+            n = abi.mtdao_stats_scratch_bytes(self.cfg)
+            self._stats_scratch = torch.empty(n, dtype=torch.uint8, device=self.x.device)
+        return abi.mtdao_sync_stats(self.handle, mask, self._stats_scratch.data_ptr(),
+                                    self._stats_scratch.numel(), _stream())
+
     @property
     def step_count(self) -> int:
         return abi.mtdao_step_count(self.handle)

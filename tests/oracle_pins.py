@@ -548,6 +548,53 @@ def pin_outer_nesterov_is_torch_sgd_nesterov():
     assert events == T // 4
 
 
+def pin_state_stats_definitions():
+    """Averaging diagnostics: a hand example, identical rows (variance 0,
+    cosine 1), opposite rows (mean 0, variance = ||S^0||^2), and the
+    identity var = mean_m ||c^m||^2 - ||cbar||^2 on random rows; with outer
+    parameters the vectors are the pseudo-gradients x_outer - x^m."""
+    a = np.array([[1.0, 2.0], [3.0, 4.0]])
+    st = oracle.state_stats(a, "f64")
+    assert np.allclose(st, [13.0, 2.0, 0.0, 0.0, 5.0, 25.0, 8.0, 18.0], rtol=0, atol=1e-12), st
+    rng = np.random.default_rng(32)
+    r = rng.normal(0, 1, 50)
+    st = oracle.state_stats(np.tile(r, (3, 1)), "f64")
+    _close(st[[4, 5, 6, 7, 8, 9]], [r @ r] * 6, 1e-12, 0, "identical rows")
+    assert abs(st[1]) < 1e-12 * (r @ r)
+    st = oracle.state_stats(np.stack([r, -r]), "f64")
+    assert abs(st[0]) < 1e-20 and abs(st[1] - r @ r) < 1e-12 * (r @ r)
+    b = rng.normal(0, 1, (5, 40))
+    st = oracle.state_stats(b, "f64")
+    _close(st[1], (b * b).sum(axis=1).mean() - st[0], 1e-10, 0, "variance identity")
+    _close(st[4 + 5:], b @ b.mean(axis=0), 1e-12, 1e-14, "dots")
+    xo = rng.normal(0, 1, 40).astype(np.float32)
+    st = oracle.state_stats(b, "f64", xo)
+    pg = xo.astype(np.float64) - b
+    _close(st[0], ((xo - b.mean(axis=0)) ** 2).sum(), 1e-12, 0, "pseudo-gradient mean")
+    _close(st[2], float(xo.astype(np.float64) @ xo.astype(np.float64)), 1e-12, 0, "outer norm")
+    _close(st[4:9], (pg * pg).sum(axis=1), 1e-12, 0, "pseudo-gradient norms")
+    _close(st[9:14], pg @ pg.mean(axis=0), 1e-12, 1e-14, "pseudo-gradient dots with their mean")
+    _close(st[1], ((pg - pg.mean(axis=0)) ** 2).sum() / 5, 1e-12, 0, "pseudo-gradient variance")
+
+
+def pin_cross_worker_variance_of_local_momentum():
+    """Section 2.1 / Appendix derivation, measured with the diagnostic:
+    from a synchronised momentum, K local steps of iid N(0, sigma^2)
+    gradients (independent across workers) give a cross-worker variance of
+    (1 - 1/M) P (1-b)/(1+b) (1 - b^{2K}) sigma^2 in expectation."""
+    rng = np.random.default_rng(33)
+    M, P, H, sigma, b = 8, 1 << 16, 32, 0.3, f32(0.9)
+    cfg = _cfg("sgdm", (b,), (0.5,), x_dtype="f32", g_dtype="f32", m_dtype="f64", period_x=0,
+               period_u=(0,), period_v=0)
+    st = oracle.new_state(cfg, np.zeros(P, dtype=np.float32), M)
+    for s in range(1, H + 1):
+        oracle.local_step(cfg, st, (sigma * rng.standard_normal((M, P))).astype(np.float32), s, 0.0)
+    stats = oracle.sync_stats(cfg, st, 0b10)
+    want = (1 - 1 / M) * P * (1 - b) / (1 + b) * (1 - b ** (2 * H)) * sigma ** 2
+    assert abs(stats[1][1] / want - 1) < 0.02, (stats[1][1], want)
+    assert np.all(st.u[0] == st.u[0][0]), "averaged after the diagnostics"
+
+
 # ----------------------------------------------------------------- P9, P11 (paper numbers)
 
 

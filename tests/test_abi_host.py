@@ -362,3 +362,32 @@ def test_binding_struct_layout_matches_header(tmp_path):
             assert (fld.offset, fld.size) == (int(parts[2]), int(parts[3])), line
             seen += 1
     assert seen == sum(len(p._fields_) for p in structs.values())
+
+
+def test_sync_stats_host_rules():
+    cfg = good_cfg()
+    n = abi.mtdao_stats_scratch_bytes(cfg)
+    assert 0 < n < 64 << 20
+    h = _fake_handle(cfg)
+    try:
+        with pytest.raises(abi.MtdaoError) as e:
+            abi.mtdao_sync_stats(h, 1, None, 0, None)
+        assert e.value.code == abi.MTDAO_ERR_WORKSPACE
+        with pytest.raises(abi.MtdaoError) as e:
+            abi.mtdao_sync_stats(h, 1, (1 << 44) + 64, n, None)
+        assert e.value.code == abi.MTDAO_ERR_ALIGN
+        with pytest.raises(abi.MtdaoError) as e:
+            abi.mtdao_sync_stats(h, 1 << 4, 1 << 44, n, None)
+        assert e.value.code == abi.MTDAO_ERR_INVALID_ARG
+        applied, st = abi.mtdao_sync_stats(h, 0, 1 << 44, n, None)  # nothing due: no launch
+        assert applied == 0 and np.all(np.isnan(st))
+    finally:
+        abi.mtdao_destroy(h)
+    big = good_cfg(replicas=17)
+    h = _fake_handle(big)
+    try:
+        with pytest.raises(abi.MtdaoError) as e:
+            abi.mtdao_sync_stats(h, 1, 1 << 44, abi.mtdao_stats_scratch_bytes(big), None)
+        assert e.value.code == abi.MTDAO_ERR_INVALID_ARG and "16" in abi.mtdao_last_error(h)
+    finally:
+        abi.mtdao_destroy(h)

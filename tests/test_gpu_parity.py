@@ -511,3 +511,67 @@ def test_outer_nesterov_full_size_bench_workload():
     # the outer rows are [P]; compare them on the sample too
     compare(w, g.opt, OracleResult(o.state, o.masks, idx), "nesterov-full")
     free(g)
+
+
+# ------------------------------------------------------------ averaging diagnostics
+
+
+def _stats_case(name, outer=None, steps=None):
+    w = synth.small_variant(synth.WORKLOADS[name], 50_000, tail=8)
+    w = w.replace(replicas=min(w.replicas, 16), steps=steps or w.steps)
+    return w
+
+
+@pytest.mark.parametrize("name,outer", [("adam_n3_k4_p16m", None), ("adopt_n2_k8_p124m_bf16", None),
+                                        ("sgdm_n2_k16_p354m_clip", None), ("adam_n3_k4_p16m", (0.7, 0.9)),
+                                        ("adopt_n2_k8_p124m_bf16", (0.7, 0.9))],
+                         ids=["adam", "adopt_bf16", "sgdm_k16", "adam_nesterov", "adopt_bf16_nesterov"])
+def test_sync_stats_against_oracle(name, outer):
+    """mtdao_sync_stats: averaged states bit-identical to mtdao_sync, and the
+    diagnostics of every averaged state equal the oracle's on the same
+    pre-average values (fp32: 1e-5 relative; bf16 x: rounding flips of x
+    shift the worker differences by a bf16 ulp, bound 2e-3)."""
+    w = _stats_case(name)
+    w = w.replace(period_x=4, period_u=(6,) * w.n_moments, period_v=8, steps=24)
+    log(f"case stats {w.name} K={w.replicas} outer={outer}")
+    d = torch.device("cuda:0")
+    dev = DeviceInputs(w, d)
+    from gpu_harness import gpu_config, oracle_cfg, OracleResult
+    a = MtdaoOptimizer(gpu_config(w, 0, outer), d, x0=dev.x0_row())
+    b = MtdaoOptimizer(gpu_config(w, 0, outer), d, x0=dev.x0_row())
+    ocfg = oracle_cfg(w, outer)
+    ost = oracle.new_state(ocfg, synth.host_x0_row(w), w.replicas)
+    gdt = torch.bfloat16 if w.grad_dtype == "bf16" else torch.float32
+    grads = torch.empty((w.replicas, w.numel), dtype=gdt, device=d)
+    checked = 0
+    for s in _steps(w):
+        dev.grads_into(s, grads)
+        a.step(grads, w.lr, w.adopt_clip_value(s))
+        b.step(grads, w.lr, w.adopt_clip_value(s))
+        ma = a.sync()
+        mb, stats = b.sync_stats()
+        oracle.local_step(ocfg, ost, synth.host_grad_rows(w, s), s, w.lr, w.adopt_clip_value(s),
+                          oracle.clip_scales(ocfg, synth.host_grad_rows(w, s)))
+        ostats = oracle.sync_stats(ocfg, ost, oracle.schedule(ocfg, s))
+        assert ma == mb == oracle.schedule(ocfg, s)
+        for sid in range(abi.MTDAO_MAX_N + 2):
+            if sid not in ostats:
+                assert np.all(np.isnan(stats[sid])), (s, sid)
+                continue
+            K = w.replicas
+            got = np.concatenate([stats[sid][:3], stats[sid][4:4 + K], stats[sid][20:20 + K]])
+            want = np.concatenate([ostats[sid][:3], ostats[sid][4:4 + K], ostats[sid][4 + K:4 + 2 * K]])
+            tol = 2e-3 if (sid == 0 and w.param_dtype == "bf16") else 1e-5
+            scale = np.maximum(np.abs(want), np.abs(want).max() * 1e-6)
+            err = np.max(np.abs(got - want) / scale)
+            assert err <= tol, (s, sid, err, got[:3], want[:3])
+            checked += 1
+    torch.cuda.synchronize()
+    assert checked >= 6
+    for p, q in zip(a.states(), b.states()):
+        assert torch.equal(p, q)
+    if outer is not None:
+        assert torch.equal(a.x_outer, b.x_outer) and torch.equal(a.x_outer_mom, b.x_outer_mom)
+    compare(w, b, OracleResult(ost, [], None), f"stats-{name}")
+    a.close()
+    b.close()

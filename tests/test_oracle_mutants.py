@@ -76,6 +76,9 @@ MUTANTS = [
     ("outer_plain_momentum", "(double)xo[p] - lr * (d + m_ * (double)b[p]);", "(double)xo[p] - lr * ((double)b[p]);", 0),
     ("outer_gradient_sign", "const double d = (double)xo[p] - xbar;", "const double d = xbar - (double)xo[p];", 0),
     ("outer_no_momentum", "const double bn = m_ * (double)b[p] + d;", "const double bn = d;", 0),
+    ("stats_variance_not_centered", "out[1] += (c - cbar) * (c - cbar);", "out[1] += c * c;", 0),
+    ("stats_pseudo_gradient_sign", "cbar += xo ? (double)xo[p] - v : v;", "cbar += xo ? v - (double)xo[p] : v;", 0),
+    ("stats_dot_uses_norm", "out[4 + K + m] += c * cbar;", "out[4 + K + m] += c * c;", 0),
     ("f32_store_truncates", "float f = (float)a;\n    ((float*)p)[i] = f;",
      "float f = (float)a;\n    if ((double)f > a && f > 0) f = nextafterf(f, 0.0f);\n    ((float*)p)[i] = f;", 0),
 ]
