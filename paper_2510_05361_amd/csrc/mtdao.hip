@@ -612,8 +612,10 @@ int32_t mtdao_sync(mtdao_handle* h, uint32_t mask, uint32_t* applied_mask, void*
     return fail(&h->err, MTDAO_ERR_INVALID_ARG,
                 "with sync_order MOMENTA_IN_STEP the moments are averaged inside mtdao_step_sync (mask 0x%x)", m);
   if (applied_mask) *applied_mask = m;
-  if (m == 0 || c.numel == 0 || c.replicas == 1) return MTDAO_OK;  // K = 1: the mean is the row
-  launch_means(h, m, reinterpret_cast<hipStream_t>(hip_stream));
+  // K = 1: the mean is the row; only an outer step on x still has work
+  const uint32_t work = c.replicas > 1 ? m : (h->x_outer ? (m & 1u) : 0u);
+  if (work == 0 || c.numel == 0) return MTDAO_OK;
+  launch_means(h, work, reinterpret_cast<hipStream_t>(hip_stream));
   return hip_check(&h->err, hipGetLastError(), "mtdao_sync launch");
 }
 
@@ -717,15 +719,17 @@ int32_t mtdao_step_sync(mtdao_handle* h, const void* grads, float lr, float adop
   if (c.numel == 0) return MTDAO_OK;
   hipStream_t st = reinterpret_cast<hipStream_t>(hip_stream);
   const StepParams p = prepare_step(h, grads, lr, adopt_clip, s, st);
+  // K = 1: the mean is the row; only an outer step on x still has work
+  const uint32_t work = c.replicas > 1 ? m : (h->x_outer ? (m & 1u) : 0u);
   if (adopt_first_update(c, s)) {
     launch_adopt_first(h, grads, st);
-    if (m != 0 && c.replicas > 1) launch_means(h, m, st);
-  } else if (m == 0 || c.replicas == 1) {
+    if (work != 0) launch_means(h, work, st);
+  } else if (work == 0) {
     launch_step(c, p, step_vec_width(c), st);
-  } else if (c.sync_order == MTDAO_SYNC_MOMENTA_IN_STEP && (m & ~1u) != 0) {
-    launch_sgdm_averaged_momenta(c, p, step_vec_width(c), m, st);
+  } else if (c.sync_order == MTDAO_SYNC_MOMENTA_IN_STEP && (work & ~1u) != 0) {
+    launch_sgdm_averaged_momenta(c, p, step_vec_width(c), work, st);
   } else {
-    launch_step_sync(c, p, step_vec_width(c), m, st);
+    launch_step_sync(c, p, step_vec_width(c), work, st);
   }
   return hip_check(&h->err, hipGetLastError(), "mtdao_step_sync launch");
 }

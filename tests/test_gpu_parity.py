@@ -575,3 +575,18 @@ def test_sync_stats_against_oracle(name, outer):
     compare(w, b, OracleResult(ost, [], None), f"stats-{name}")
     a.close()
     b.close()
+
+
+@pytest.mark.parametrize("fused", [False, True], ids=["separate", "fused"])
+def test_outer_nesterov_single_replica(fused):
+    """K = 1: averaging is the identity, but the Nesterov outer step still
+    moves the outer parameters and restarts the worker from them."""
+    w = synth.small_variant(synth.WORKLOADS["adam_n3_k4_p16m"], 20_000, tail=4).replace(
+        replicas=1, steps=24, period_x=3)
+    g = run_gpu(w, _steps(w), outer=NESTEROV, fused=fused)
+    o = run_oracle(w, _steps(w), outer=NESTEROV)
+    assert g.masks == o.masks
+    compare(w, g.opt, o, f"nesterov-k1-{fused}")
+    avg = run_gpu(w, _steps(w), fused=fused)
+    assert not torch.equal(avg.opt.x, g.opt.x), "the outer step must act at K = 1"
+    free(g, avg)
