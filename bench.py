@@ -154,11 +154,22 @@ def cpu_baseline(w, target_s: float = 12.0):
     syncs_per_step = (1.0 / w.period_x if w.period_x else 0.0) + sum(
         1.0 / h for h in w.period_u if h) + (1.0 / w.period_v if (w.has_v and w.period_v) else 0.0)
     t = t_step + syncs_per_step * t_mean
+    cpu = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    cpu = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
     return {
         "value": w.replicas * n / t,
         "unit": "element-updates/s",
         "cores": 1,
         "kind": "oracle",
+        "cpu_model": cpu,
+        "host_cpus": os.cpu_count(),
         "sample": (f"{n} elements x {w.replicas} replicas of {w.name}: {steps} local steps "
                    f"({el:.1f} s{', clip norms included' if scale is not None else ''}) + one replica "
                    f"mean, sync amortised at {syncs_per_step:.4f} state-syncs/step; single thread"),
