@@ -403,6 +403,93 @@ __global__ __launch_bounds__(kBlock) void k_local_step_sync(StepParams p, uint32
   }
 }
 
+// The same fused step + mean with one wavefront per replica (blockDim =
+// 64 K, 1 < K <= kWaveMaxK): lane l of wave m updates elements
+// [e, e + V) of replica m, e = tile 64 V + l V, exactly like the plain step,
+// so every replica keeps its own loads in flight.  For each due state the
+// updated values pass through LDS; wave 0 forms S^0 + (sum_{m>=1}(S^m -
+// S^0)) / K in replica order (the arithmetic of k_replica_mean, bit for
+// bit), applies the OuterOpt to x, and every wave stores the mean to its
+// row.  Barriers are reached by all threads, also in the row tail.
+constexpr int kWaveMaxK = 16;
+
+template <int FORM, int N, typename XT, typename GT, int V, int NTM, int ORDER>
+__global__ __launch_bounds__(64 * kWaveMaxK) void k_local_step_sync_waves(StepParams p, uint32_t mask, int32_t K) {
+  constexpr bool NTL = (NTM & 1) != 0, NTS = (NTM & 2) != 0;
+  constexpr int NS = 2 + N;  // x, u^1..u^N, v
+  __shared__ float lds[kWaveMaxK][64 * V];
+  const int32_t m = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  XT* __restrict__ x = reinterpret_cast<XT*>(p.x);
+  const GT* __restrict__ g = reinterpret_cast<const GT*>(p.g);
+  const float kf = (float)K;
+  const float sc = (FORM != kAdopt && p.scale != nullptr) ? p.scale[m] : 1.0f;
+
+  for (int64_t tile = blockIdx.x; tile < p.tiles; tile += gridDim.x) {
+    const int64_t e = tile * (int64_t)(64 * V) + (int64_t)lane * V;
+    const bool in = e < p.P;
+    const int64_t r = (int64_t)m * p.P + e;
+    float val[NS][V];  // updated x, u^j, v of this lane's elements
+    if (in) {
+      float gv[V], uv[N][V];
+      load_v<GT, V, NTL>(g, r, gv);
+      load_v<XT, V, NTL>(x, r, val[0]);
+#pragma unroll
+      for (int j = 0; j < N; ++j) load_v<float, V, NTL>(p.u[j], r, uv[j]);
+      if constexpr (FORM != kSgdm) load_v<float, V, NTL>(p.v, r, val[NS - 1]);
+#pragma unroll
+      for (int t = 0; t < V; ++t) {
+        float uu[N];
+#pragma unroll
+        for (int j = 0; j < N; ++j) uu[j] = uv[j][t];
+        float vt = (FORM != kSgdm) ? val[NS - 1][t] : 0.0f;
+        update_element<FORM, N, ORDER>(p, sc, gv[t], val[0][t], uu, vt);
+        val[0][t] = as_stored<XT>(val[0][t]);
+#pragma unroll
+        for (int j = 0; j < N; ++j) val[1 + j][t] = uu[j];
+        val[NS - 1][t] = vt;
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < NS; ++k) {
+      if (FORM == kSgdm && k == NS - 1) continue;
+      const bool due = ((mask >> k) & 1u) != 0;
+      if (!due) {
+        if (!in) continue;
+        if (k == 0) store_v<XT, V, NTS>(x, r, val[0]);
+        else if (k == NS - 1) store_v<float, V, NTS>(p.v, r, val[k]);
+        else store_v<float, V, NTS>(p.u[k - 1], r, val[k]);
+        continue;
+      }
+#pragma unroll
+      for (int t = 0; t < V; ++t) lds[m][lane * V + t] = val[k][t];
+      __syncthreads();
+      if (m == 0 && in) {
+        float mean[V];
+#pragma unroll
+        for (int t = 0; t < V; ++t) {
+          const float s0 = lds[0][lane * V + t];
+          float d = 0.0f;
+          for (int32_t q = 1; q < K; ++q) d += lds[q][lane * V + t] - s0;
+          mean[t] = s0 + d / kf;
+        }
+        if (k == 0) outer_step<V>(p.outer, e, mean);
+#pragma unroll
+        for (int t = 0; t < V; ++t) lds[0][lane * V + t] = mean[t];
+      }
+      __syncthreads();
+      if (in) {
+        float mean[V];
+#pragma unroll
+        for (int t = 0; t < V; ++t) mean[t] = lds[0][lane * V + t];
+        if (k == 0) store_v<XT, V, NTS>(x, r, mean);
+        else if (k == NS - 1) store_v<float, V, NTS>(p.v, r, mean);
+        else store_v<float, V, NTS>(p.u[k - 1], r, mean);
+      }
+      __syncthreads();
+    }
+  }
+}
+
 // Probabilistic SGDM variant (Algorithm 4): the first moments due in mask
 // are averaged over the replicas BEFORE the update direction uses them, so
 // every replica steps with the averaged momentum; x is updated and, when

@@ -241,6 +241,22 @@ void launch_step_sync(const mtdao_config& c, StepParams p, int V, uint32_t mask,
     constexpr int FORM = decltype(form)::value, N = decltype(n)::value, VV = decltype(vw)::value;
     using XT = typename decltype(xt)::type;
     using GT = typename decltype(gt)::type;
+    if (c.replicas > 1 && c.replicas <= kWaveMaxK) {
+      // one wavefront per replica
+      const int64_t per = (int64_t)64 * VV;
+      p.tiles = (p.P + per - 1) / per;
+      const dim3 grid = grid_for(p.tiles, 1), block(64 * c.replicas);
+      if constexpr (FORM == kAdopt) {
+        if (c.adopt_order == MTDAO_ADOPT_CUR) {
+          hipLaunchKernelGGL((k_local_step_sync_waves<FORM, N, XT, GT, VV, kStepNT, kCur>), grid, block, 0, st, p, mask,
+                             c.replicas);
+          return;
+        }
+      }
+      hipLaunchKernelGGL((k_local_step_sync_waves<FORM, N, XT, GT, VV, kStepNT, kPrev>), grid, block, 0, st, p, mask,
+                         c.replicas);
+      return;
+    }
     const int64_t per = (int64_t)kBlock * VV;
     p.tiles = (p.P + per - 1) / per;
     const dim3 grid = grid_for(p.tiles, 1);

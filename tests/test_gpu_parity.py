@@ -590,3 +590,27 @@ def test_outer_nesterov_single_replica(fused):
     avg = run_gpu(w, _steps(w), fused=fused)
     assert not torch.equal(avg.opt.x, g.opt.x), "the outer step must act at K = 1"
     free(g, avg)
+
+
+# ------------------------------------------------------------ degenerate sizes
+
+
+@pytest.mark.parametrize("P,K", [(1, 3), (3, 2), (63, 5), (64, 4), (1029, 17), (200, 1024)],
+                         ids=["one_element", "three", "below_a_wave", "one_wave", "k17_thread_fused", "k_max"])
+@pytest.mark.parametrize("form", ["adam", "adopt", "sgdm"])
+def test_degenerate_sizes(P, K, form):
+    """Tiny rows (one element, shorter than a wavefront), K = 17 (the fused
+    kernel that walks the replicas per thread) and K = MTDAO_MAX_REPLICAS:
+    separate and fused entry points against the oracle, bit-identical to
+    each other."""
+    base = {"adam": "adam_n3_k4_p16m", "adopt": "adopt_n2_k8_p124m_bf16", "sgdm": "sgdm_n2_k16_p354m_clip"}[form]
+    w = synth.WORKLOADS[base].replace(tensors=(synth.TensorSpec("t", P, "matrix"),), replicas=K, steps=10,
+                                      period_x=2, period_u=(3,) * synth.WORKLOADS[base].n_moments, period_v=5)
+    g = run_gpu(w, _steps(w))
+    f = run_gpu(w, _steps(w), fused=True)
+    o = run_oracle(w, _steps(w))
+    assert g.masks == f.masks == o.masks
+    compare(w, g.opt, o, f"tiny-{form}-{P}-{K}")
+    for p, q in zip(g.opt.states(), f.opt.states()):
+        assert torch.equal(p, q)
+    free(g, f)
