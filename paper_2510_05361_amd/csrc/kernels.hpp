@@ -461,26 +461,26 @@ __global__ __launch_bounds__(64 * kWaveMaxK) void k_local_step_sync_waves(StepPa
         continue;
       }
 #pragma unroll
-      for (int t = 0; t < V; ++t) lds[m][lane * V + t] = val[k][t];
+      for (int t = 0; t < V; ++t) lds[m][t * 64 + lane] = val[k][t];
       __syncthreads();
       if (m == 0 && in) {
         float mean[V];
 #pragma unroll
         for (int t = 0; t < V; ++t) {
-          const float s0 = lds[0][lane * V + t];
+          const float s0 = lds[0][t * 64 + lane];
           float d = 0.0f;
-          for (int32_t q = 1; q < K; ++q) d += lds[q][lane * V + t] - s0;
+          for (int32_t q = 1; q < K; ++q) d += lds[q][t * 64 + lane] - s0;
           mean[t] = s0 + d / kf;
         }
         if (k == 0) outer_step<V>(p.outer, e, mean);
 #pragma unroll
-        for (int t = 0; t < V; ++t) lds[0][lane * V + t] = mean[t];
+        for (int t = 0; t < V; ++t) lds[0][t * 64 + lane] = mean[t];
       }
       __syncthreads();
       if (in) {
         float mean[V];
 #pragma unroll
-        for (int t = 0; t < V; ++t) mean[t] = lds[0][lane * V + t];
+        for (int t = 0; t < V; ++t) mean[t] = lds[0][t * 64 + lane];
         if (k == 0) store_v<XT, V, NTS>(x, r, mean);
         else if (k == NS - 1) store_v<float, V, NTS>(p.v, r, mean);
         else store_v<float, V, NTS>(p.u[k - 1], r, mean);
