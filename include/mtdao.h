@@ -207,8 +207,9 @@ int32_t mtdao_local_step(mtdao_handle* h, const void* grads, float lr, float ado
  * the schedule (states whose period divides s); any other value is taken as
  * the explicit set of states to average (e.g. the Bernoulli draws of the
  * probabilistic variant, Algorithm 4, made by the caller).  Every element of
- * every selected state becomes S^0 + (sum_{m>=1} (S^m - S^0)) / K computed
- * in fp32 and is written to all K rows, so averaging identical rows is an
+ * every selected state becomes S^0 + (sum_{m>=1} (S^m - S^0)) / K, the
+ * differences summed in fp64 and the result rounded once to the storage
+ * type, and is written to all K rows, so averaging identical rows is an
  * exact no-op and a repeated call at the same s changes nothing.
  * applied_mask (may be NULL) receives the set actually averaged. */
 int32_t mtdao_sync(mtdao_handle* h, uint32_t mask, uint32_t* applied_mask, void* hip_stream);

@@ -292,6 +292,17 @@ __device__ __forceinline__ float as_stored(float a) {
   else return a;
 }
 
+// The replica mean of one element, shared by every averaging kernel:
+// S^0 + (sum_{m>=1} (S^m - S^0)) / K, the differences summed in fp64 in
+// replica order and the result rounded to fp32 once.  (An fp32 running sum
+// loses up to about (K - 1) 2^-24 of the rows' spread, which at large K is
+// more than the mean itself carries when the rows nearly cancel.)  Identical
+// rows give S^0 back exactly.  rk = 1 / K in fp64.
+__device__ __forceinline__ void mean_add(double& d, float a, float s0) { d += (double)a - (double)s0; }
+__device__ __forceinline__ float mean_of(float s0, double d, double rk) {
+  return (float)__builtin_fma(d, rk, (double)s0);
+}
+
 // Local update of every replica followed by the replica mean of the states
 // in `mask` (bit 0 = x, bit j = u^j, bit N+1 = v), in one pass.  A thread
 // owns V columns of every replica: it updates replica 0..K-1 in order,
@@ -311,18 +322,19 @@ __global__ __launch_bounds__(kBlock) void k_local_step_sync(StepParams p, uint32
   const bool sync_v = FORM != kSgdm && ((mask >> (N + 1)) & 1u) != 0;
   XT* __restrict__ x = reinterpret_cast<XT*>(p.x);
   const GT* __restrict__ g = reinterpret_cast<const GT*>(p.g);
-  const float kf = (float)K;
+  const double rk = 1.0 / (double)K;
 
   for (int64_t tile = blockIdx.x; tile < p.tiles; tile += gridDim.x) {
     const int64_t e = tile * (int64_t)(kBlock * V) + (int64_t)threadIdx.x * V;
     if (e >= p.P) continue;
-    float x0[V], dx[V], u0[N][V], du[N][V], v0[V], dv[V];
+    float x0[V], u0[N][V], v0[V];
+    double dx[V], du[N][V], dv[V];
 #pragma unroll
     for (int t = 0; t < V; ++t) {
-      dx[t] = 0.0f;
-      dv[t] = 0.0f;
+      dx[t] = 0.0;
+      dv[t] = 0.0;
 #pragma unroll
-      for (int j = 0; j < N; ++j) du[j][t] = 0.0f;
+      for (int j = 0; j < N; ++j) du[j][t] = 0.0;
     }
     for (int32_t m = 0; m < K; ++m) {
       const int64_t r = (int64_t)m * p.P + e;
@@ -350,7 +362,7 @@ __global__ __launch_bounds__(kBlock) void k_local_step_sync(StepParams p, uint32
 #pragma unroll
         for (int t = 0; t < V; ++t) {
           if (m == 0) x0[t] = xv[t];
-          else dx[t] += xv[t] - x0[t];
+          else mean_add(dx[t], xv[t], x0[t]);
         }
       } else {
         store_v<XT, V, NTS>(x, r, xv);
@@ -361,7 +373,7 @@ __global__ __launch_bounds__(kBlock) void k_local_step_sync(StepParams p, uint32
 #pragma unroll
           for (int t = 0; t < V; ++t) {
             if (m == 0) u0[j][t] = uv[j][t];
-            else du[j][t] += uv[j][t] - u0[j][t];
+            else mean_add(du[j][t], uv[j][t], u0[j][t]);
           }
         } else {
           store_v<float, V, NTS>(p.u[j], r, uv[j]);
@@ -372,7 +384,7 @@ __global__ __launch_bounds__(kBlock) void k_local_step_sync(StepParams p, uint32
 #pragma unroll
           for (int t = 0; t < V; ++t) {
             if (m == 0) v0[t] = vv[t];
-            else dv[t] += vv[t] - v0[t];
+            else mean_add(dv[t], vv[t], v0[t]);
           }
         } else {
           store_v<float, V, NTS>(p.v, r, vv);
@@ -382,7 +394,7 @@ __global__ __launch_bounds__(kBlock) void k_local_step_sync(StepParams p, uint32
     // the means, written to every replica row
     if (sync_x) {
 #pragma unroll
-      for (int t = 0; t < V; ++t) x0[t] = x0[t] + dx[t] / kf;
+      for (int t = 0; t < V; ++t) x0[t] = mean_of(x0[t], dx[t], rk);
       outer_step<V>(p.outer, e, x0);
       for (int32_t m = 0; m < K; ++m) store_v<XT, V, NTS>(x, (int64_t)m * p.P + e, x0);
     }
@@ -390,13 +402,13 @@ __global__ __launch_bounds__(kBlock) void k_local_step_sync(StepParams p, uint32
     for (int j = 0; j < N; ++j) {
       if (!sync_u[j]) continue;
 #pragma unroll
-      for (int t = 0; t < V; ++t) u0[j][t] = u0[j][t] + du[j][t] / kf;
+      for (int t = 0; t < V; ++t) u0[j][t] = mean_of(u0[j][t], du[j][t], rk);
       for (int32_t m = 0; m < K; ++m) store_v<float, V, NTS>(p.u[j], (int64_t)m * p.P + e, u0[j]);
     }
     if constexpr (FORM != kSgdm) {
       if (sync_v) {
 #pragma unroll
-        for (int t = 0; t < V; ++t) v0[t] = v0[t] + dv[t] / kf;
+        for (int t = 0; t < V; ++t) v0[t] = mean_of(v0[t], dv[t], rk);
         for (int32_t m = 0; m < K; ++m) store_v<float, V, NTS>(p.v, (int64_t)m * p.P + e, v0);
       }
     }
@@ -410,18 +422,20 @@ __global__ __launch_bounds__(kBlock) void k_local_step_sync(StepParams p, uint32
 // updated values pass through LDS; wave 0 forms S^0 + (sum_{m>=1}(S^m -
 // S^0)) / K in replica order (the arithmetic of k_replica_mean, bit for
 // bit), applies the OuterOpt to x, and every wave stores the mean to its
-// row.  Barriers are reached by all threads, also in the row tail.
+// row.  Barriers are reached by all threads, also in the row tail.  The
+// register budget is held to 8 waves per SIMD, so two 16-wave workgroups
+// share a CU and one's mean phase overlaps the other's streaming.
 constexpr int kWaveMaxK = 16;
 
 template <int FORM, int N, typename XT, typename GT, int V, int NTM, int ORDER>
-__global__ __launch_bounds__(64 * kWaveMaxK) void k_local_step_sync_waves(StepParams p, uint32_t mask, int32_t K) {
+__global__ __launch_bounds__(64 * kWaveMaxK) __attribute__((amdgpu_waves_per_eu(8))) void k_local_step_sync_waves(StepParams p, uint32_t mask, int32_t K) {
   constexpr bool NTL = (NTM & 1) != 0, NTS = (NTM & 2) != 0;
   constexpr int NS = 2 + N;  // x, u^1..u^N, v
   __shared__ float lds[kWaveMaxK][64 * V];
   const int32_t m = threadIdx.x >> 6, lane = threadIdx.x & 63;
   XT* __restrict__ x = reinterpret_cast<XT*>(p.x);
   const GT* __restrict__ g = reinterpret_cast<const GT*>(p.g);
-  const float kf = (float)K;
+  const double rk = 1.0 / (double)K;
   const float sc = (FORM != kAdopt && p.scale != nullptr) ? p.scale[m] : 1.0f;
 
   for (int64_t tile = blockIdx.x; tile < p.tiles; tile += gridDim.x) {
@@ -468,9 +482,10 @@ __global__ __launch_bounds__(64 * kWaveMaxK) void k_local_step_sync_waves(StepPa
 #pragma unroll
         for (int t = 0; t < V; ++t) {
           const float s0 = lds[0][t * 64 + lane];
-          float d = 0.0f;
-          for (int32_t q = 1; q < K; ++q) d += lds[q][t * 64 + lane] - s0;
-          mean[t] = s0 + d / kf;
+          double d = 0.0;
+#pragma unroll 1
+          for (int32_t q = 1; q < K; ++q) mean_add(d, lds[q][t * 64 + lane], s0);
+          mean[t] = mean_of(s0, d, rk);
         }
         if (k == 0) outer_step<V>(p.outer, e, mean);
 #pragma unroll
@@ -507,17 +522,18 @@ __global__ __launch_bounds__(kBlock) void k_sgdm_averaged_momenta(StepParams p, 
   for (int j = 0; j < N; ++j) sync_u[j] = ((mask >> (j + 1)) & 1u) != 0;
   XT* __restrict__ x = reinterpret_cast<XT*>(p.x);
   const GT* __restrict__ g = reinterpret_cast<const GT*>(p.g);
-  const float kf = (float)K;
+  const double rk = 1.0 / (double)K;
 
   for (int64_t tile = blockIdx.x; tile < p.tiles; tile += gridDim.x) {
     const int64_t e = tile * (int64_t)(kBlock * V) + (int64_t)threadIdx.x * V;
     if (e >= p.P) continue;
     // pass 1: u^j of every replica; due ones become their replica mean
-    float u0[N][V], du[N][V];
+    float u0[N][V];
+    double du[N][V];
 #pragma unroll
     for (int j = 0; j < N; ++j)
 #pragma unroll
-      for (int t = 0; t < V; ++t) du[j][t] = 0.0f;
+      for (int t = 0; t < V; ++t) du[j][t] = 0.0;
     for (int32_t m = 0; m < K; ++m) {
       const int64_t r = (int64_t)m * p.P + e;
       float gv[V], uv[N][V];
@@ -537,7 +553,7 @@ __global__ __launch_bounds__(kBlock) void k_sgdm_averaged_momenta(StepParams p, 
 #pragma unroll
           for (int t = 0; t < V; ++t) {
             if (m == 0) u0[j][t] = uv[j][t];
-            else du[j][t] += uv[j][t] - u0[j][t];
+            else mean_add(du[j][t], uv[j][t], u0[j][t]);
           }
         } else {
           store_v<float, V, false>(p.u[j], r, uv[j]);
@@ -548,13 +564,14 @@ __global__ __launch_bounds__(kBlock) void k_sgdm_averaged_momenta(StepParams p, 
     for (int j = 0; j < N; ++j) {
       if (!sync_u[j]) continue;
 #pragma unroll
-      for (int t = 0; t < V; ++t) u0[j][t] = u0[j][t] + du[j][t] / kf;
+      for (int t = 0; t < V; ++t) u0[j][t] = mean_of(u0[j][t], du[j][t], rk);
       for (int32_t m = 0; m < K; ++m) store_v<float, V, NTS>(p.u[j], (int64_t)m * p.P + e, u0[j]);
     }
     // pass 2: direction with the averaged (due) or local (not due) moments
-    float x0[V], dx[V];
+    float x0[V];
+    double dx[V];
 #pragma unroll
-    for (int t = 0; t < V; ++t) dx[t] = 0.0f;
+    for (int t = 0; t < V; ++t) dx[t] = 0.0;
     for (int32_t m = 0; m < K; ++m) {
       const int64_t r = (int64_t)m * p.P + e;
       float gv[V], xv[V], uv[N][V];
@@ -582,7 +599,7 @@ __global__ __launch_bounds__(kBlock) void k_sgdm_averaged_momenta(StepParams p, 
 #pragma unroll
         for (int t = 0; t < V; ++t) {
           if (m == 0) x0[t] = xv[t];
-          else dx[t] += xv[t] - x0[t];
+          else mean_add(dx[t], xv[t], x0[t]);
         }
       } else {
         store_v<XT, V, NTS>(x, r, xv);
@@ -590,7 +607,7 @@ __global__ __launch_bounds__(kBlock) void k_sgdm_averaged_momenta(StepParams p, 
     }
     if (sync_x) {
 #pragma unroll
-      for (int t = 0; t < V; ++t) x0[t] = x0[t] + dx[t] / kf;
+      for (int t = 0; t < V; ++t) x0[t] = mean_of(x0[t], dx[t], rk);
       for (int32_t m = 0; m < K; ++m) store_v<XT, V, NTS>(x, (int64_t)m * p.P + e, x0);
     }
   }
@@ -629,22 +646,23 @@ struct MeanParams {
 };
 
 // E_m[S] for the state blockIdx.y: every element becomes
-// S^0 + (sum_{m>=1} (S^m - S^0)) / K in fp32 and is stored to all K rows.
+// S^0 + (sum_{m>=1} (S^m - S^0)) / K (mean_of) and is stored to all K rows.
 // Each thread reads the K rows of its own columns and writes them back, so
 // the in-place update has no cross-thread hazard.
 template <typename T, int V, bool NT, int U = 1>
 __global__ __launch_bounds__(kBlock) void k_replica_mean(MeanParams p) {
   T* __restrict__ s = reinterpret_cast<T*>(p.state[blockIdx.y]);
-  const float kf = (float)p.K;
+  const double rk = 1.0 / (double)p.K;
   for (int64_t tile = blockIdx.x; tile < p.tiles; tile += gridDim.x) {
     const int64_t base = tile * (int64_t)(kBlock * V * U);
-    float s0[U][V], d[U][V];
+    float s0[U][V];
+    double d[U][V];
 #pragma unroll
     for (int k = 0; k < U; ++k) {
       const int64_t e = base + ((int64_t)k * kBlock + threadIdx.x) * V;
       if (e < p.P) load_v<T, V, NT>(s, e, s0[k]);
 #pragma unroll
-      for (int t = 0; t < V; ++t) d[k][t] = 0.0f;
+      for (int t = 0; t < V; ++t) d[k][t] = 0.0;
     }
 #pragma unroll 4
     for (int32_t m = 1; m < p.K; ++m) {
@@ -655,7 +673,7 @@ __global__ __launch_bounds__(kBlock) void k_replica_mean(MeanParams p) {
         float a[V];
         load_v<T, V, NT>(s + (int64_t)m * p.P, e, a);
 #pragma unroll
-        for (int t = 0; t < V; ++t) d[k][t] += a[t] - s0[k][t];
+        for (int t = 0; t < V; ++t) mean_add(d[k][t], a[t], s0[k][t]);
       }
     }
 #pragma unroll
@@ -663,7 +681,7 @@ __global__ __launch_bounds__(kBlock) void k_replica_mean(MeanParams p) {
       const int64_t e = base + ((int64_t)k * kBlock + threadIdx.x) * V;
       if (e >= p.P) continue;
 #pragma unroll
-      for (int t = 0; t < V; ++t) s0[k][t] = s0[k][t] + d[k][t] / kf;
+      for (int t = 0; t < V; ++t) s0[k][t] = mean_of(s0[k][t], d[k][t], rk);
       if ((int32_t)blockIdx.y == p.outer_state) outer_step<V>(p.outer, e, s0[k]);
 #pragma unroll 4
       for (int32_t m = 0; m < p.K; ++m) store_v<T, V, NT>(s + (int64_t)m * p.P, e, s0[k]);
@@ -753,7 +771,7 @@ __global__ __launch_bounds__(kBlock) void k_replica_mean_stats(MeanParams p, dou
   T* __restrict__ s = reinterpret_cast<T*>(p.state[blockIdx.y]);
   const bool outer = (int32_t)blockIdx.y == p.outer_state && p.outer.xo != nullptr;
   const int32_t K = p.K;
-  const float kf = (float)K;
+  const double rk = 1.0 / (double)K;
   double a_mean = 0.0, a_var = 0.0, a_ref = 0.0, a_sq[kStatsMaxK], a_dot[kStatsMaxK];
 #pragma unroll
   for (int m = 0; m < kStatsMaxK; ++m) a_sq[m] = a_dot[m] = 0.0;
@@ -767,11 +785,11 @@ __global__ __launch_bounds__(kBlock) void k_replica_mean_stats(MeanParams p, dou
     float mean[V], xo[V];
 #pragma unroll
     for (int t = 0; t < V; ++t) {
-      float d = 0.0f;
+      double d = 0.0;
 #pragma unroll
       for (int m = 1; m < kStatsMaxK; ++m)
-        if (m < K) d += r[m][t] - r[0][t];
-      mean[t] = r[0][t] + d / kf;
+        if (m < K) mean_add(d, r[m][t], r[0][t]);
+      mean[t] = mean_of(r[0][t], d, rk);
     }
     if (outer) load_v<float, V, false>(p.outer.xo, e, xo);
 #pragma unroll
