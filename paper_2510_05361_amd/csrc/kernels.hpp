@@ -419,16 +419,18 @@ __global__ __launch_bounds__(kBlock) void k_local_step_sync(StepParams p, uint32
 // 64 K, 1 < K <= kWaveMaxK): lane l of wave m updates elements
 // [e, e + V) of replica m, e = tile 64 V + l V, exactly like the plain step,
 // so every replica keeps its own loads in flight.  For each due state the
-// updated values pass through LDS; wave 0 forms S^0 + (sum_{m>=1}(S^m -
-// S^0)) / K in replica order (the arithmetic of k_replica_mean, bit for
-// bit), applies the OuterOpt to x, and every wave stores the mean to its
+// updated values pass through LDS; the mean of column t of the tile is
+// formed by wave t mod K as S^0 + (sum_{m>=1}(S^m - S^0)) / K in replica
+// order (the arithmetic of k_replica_mean, bit for bit), the OuterOpt is
+// applied to x element by element, and every wave stores the mean to its
 // row.  Barriers are reached by all threads, also in the row tail.  The
 // register budget is held to 8 waves per SIMD, so two 16-wave workgroups
 // share a CU and one's mean phase overlaps the other's streaming.
 constexpr int kWaveMaxK = 16;
 
 template <int FORM, int N, typename XT, typename GT, int V, int NTM, int ORDER>
-__global__ __launch_bounds__(64 * kWaveMaxK) __attribute__((amdgpu_waves_per_eu(8))) void k_local_step_sync_waves(StepParams p, uint32_t mask, int32_t K) {
+__global__ __launch_bounds__(64 * kWaveMaxK) __attribute__((amdgpu_waves_per_eu(8)))
+void k_local_step_sync_waves(StepParams p, uint32_t mask, int32_t K) {
   constexpr bool NTL = (NTM & 1) != 0, NTS = (NTM & 2) != 0;
   constexpr int NS = 2 + N;  // x, u^1..u^N, v
   __shared__ float lds[kWaveMaxK][64 * V];
@@ -477,19 +479,15 @@ __global__ __launch_bounds__(64 * kWaveMaxK) __attribute__((amdgpu_waves_per_eu(
 #pragma unroll
       for (int t = 0; t < V; ++t) lds[m][t * 64 + lane] = val[k][t];
       __syncthreads();
-      if (m == 0 && in) {
-        float mean[V];
-#pragma unroll
-        for (int t = 0; t < V; ++t) {
-          const float s0 = lds[0][t * 64 + lane];
-          double d = 0.0;
-#pragma unroll 1
-          for (int32_t q = 1; q < K; ++q) mean_add(d, lds[q][t * 64 + lane], s0);
-          mean[t] = mean_of(s0, d, rk);
-        }
-        if (k == 0) outer_step<V>(p.outer, e, mean);
-#pragma unroll
-        for (int t = 0; t < V; ++t) lds[0][t * 64 + lane] = mean[t];
+      // column t (element e + t of every lane) is averaged by wave t mod K
+      for (int t = m; in && t < V; t += K) {
+        const float s0 = lds[0][t * 64 + lane];
+        double d = 0.0;
+#pragma unroll 4
+        for (int32_t q = 1; q < K; ++q) mean_add(d, lds[q][t * 64 + lane], s0);
+        float mean[1] = {mean_of(s0, d, rk)};
+        if (k == 0) outer_step<1>(p.outer, e + t, mean);
+        lds[0][t * 64 + lane] = mean[0];
       }
       __syncthreads();
       if (in) {
