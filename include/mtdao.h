@@ -216,10 +216,10 @@ int32_t mtdao_sync(mtdao_handle* h, uint32_t mask, uint32_t* applied_mask, void*
 
 /* mtdao_local_step followed by mtdao_sync(mask) in one pass over memory:
  * same arguments and same results, bit for bit (mask = MTDAO_SYNC_AUTO is
- * the schedule at the new step s).  When states are due, every element's K
- * replica rows are updated and averaged by one thread and the mean is
- * written straight to all rows, so the separate averaging pass (read and
- * write of K rows per due state) is not needed.  applied_mask (may be NULL)
+ * the schedule at the new step s).  When states are due, the K replica rows
+ * of every element are updated and averaged within one workgroup and the
+ * mean is written straight to all rows, so the separate averaging pass
+ * (read and write of K rows per due state) is not needed.  applied_mask (may be NULL)
  * receives the set averaged.  Nothing is enqueued and the step counter does
  * not move when an argument is rejected. */
 int32_t mtdao_step_sync(mtdao_handle* h, const void* grads, float lr, float adopt_clip, uint32_t mask,

@@ -4,11 +4,11 @@
 // u^1..u^N, v once and writes x, u^1..u^N, v once per element (no MFMA:
 // there is no contraction).  Every thread owns V consecutive elements of
 // one replica row per vector slot, so loads and stores are 16-byte vector
-// accesses and a 64-lane wavefront moves 1 KiB per instruction; U slots
-// per thread are issued before any of them is consumed to keep enough
-// bytes in flight per CU.  Rows are replica-major [K][P]; blockIdx.y is
-// the replica (or the state, for the mean), blockIdx.x strides over tiles
-// of 256*V*U elements of the row.
+// accesses and a 64-lane wavefront moves 1 KiB per instruction; all loads
+// of a tile are issued before any of them is consumed.  Rows are
+// replica-major [K][P]; blockIdx.y is the replica (or the state, for the
+// mean), blockIdx.x strides over tiles of 256*V*U elements of the row,
+// placed on the row by tile_elem().
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -123,6 +123,45 @@ __device__ __forceinline__ void store_v(T* __restrict__ p, int64_t e, const floa
   }
 }
 
+// ------------------------------------------------------ tile -> elements
+//
+// Workgroups are dispatched round-robin over the 8 XCDs, so with a plain
+// tile sequence XCD i works on tiles i, i + 8, ...  The HBM rate of a
+// streaming pass depends on how large a contiguous piece each XCD takes in
+// turn: pieces of 512 B - 1 KiB per stream spread the XCDs' traffic over
+// the memory channels best, 2 KiB pieces worst (about 10 % apart on MI355X
+// for the same bytes).  tile_elem() therefore splits a tile of B*V*U
+// elements into pieces of C elements and places piece j of tile t at piece
+// index ((t / 8) * R + j) * 8 + t % 8 of the row (R = pieces per tile), so
+// workgroups on one XCD still take one piece in eight and the pieces of a
+// tile are 8 C elements apart.  C = 0 keeps the tile contiguous.  Every
+// element of the row belongs to exactly one (tile, slot, thread) for
+// tiles < tiles_for<B * V * U, C>(P); elements past P are skipped by the
+// callers' bounds checks.
+template <int T, int C>
+__device__ __forceinline__ int64_t tile_elem(int64_t tile, int local) {
+  if constexpr (C == 0) {
+    return tile * (int64_t)T + local;
+  } else {
+    static_assert(T % C == 0, "a tile holds whole pieces");
+    constexpr int R = T / C;
+    const int64_t piece = ((tile >> 3) * R + local / C) * 8 + (tile & 7);
+    return piece * C + local % C;
+  }
+}
+
+// Number of tiles that cover a row of P elements under tile_elem<T, C>.
+template <int T, int C>
+__host__ __device__ constexpr int64_t tiles_for(int64_t P) {
+  if constexpr (C == 0) {
+    return (P + T - 1) / T;
+  } else {
+    const int64_t pieces = (P + C - 1) / C;
+    const int64_t per8 = 8 * (int64_t)(T / C);  // pieces covered by 8 consecutive tiles
+    return (pieces + per8 - 1) / per8 * 8;
+  }
+}
+
 // ------------------------------------------------------------ OuterOpt
 
 // Nesterov OuterOpt at an averaging event of x (xo == nullptr: plain
@@ -234,7 +273,8 @@ __device__ __forceinline__ void update_element(const StepParams& p, float sc, fl
 //   NTM        bit 0: nontemporal loads, bit 1: nontemporal stores
 //   ORDER      ADOPT normalisation order (kPrev: v from before this step)
 //   B          threads per block
-template <int FORM, int N, typename XT, typename GT, int V, int U, int NTM, int ORDER, int B = kBlock>
+//   C          elements per piece of the tile -> element map (tile_elem)
+template <int FORM, int N, typename XT, typename GT, int V, int U, int NTM, int ORDER, int B = kBlock, int C = 0>
 __global__ __launch_bounds__(B) void k_local_step(StepParams p) {
   constexpr bool NTL = (NTM & 1) != 0, NTS = (NTM & 2) != 0;
   const int64_t m = blockIdx.y;
@@ -248,12 +288,11 @@ __global__ __launch_bounds__(B) void k_local_step(StepParams p) {
   const float sc = (FORM != kAdopt && p.scale != nullptr) ? p.scale[m] : 1.0f;
 
   for (int64_t tile = blockIdx.x; tile < p.tiles; tile += gridDim.x) {
-    const int64_t base = tile * (int64_t)(B * V * U);
     float gv[U][V], xv[U][V], uv[U][N][V], vv[U][V];
     // issue every load of the tile before any arithmetic
 #pragma unroll
     for (int k = 0; k < U; ++k) {
-      const int64_t e = base + ((int64_t)k * B + threadIdx.x) * V;
+      const int64_t e = tile_elem<B * V * U, C>(tile, (k * B + (int)threadIdx.x) * V);
       if (e < p.P) {
         load_v<GT, V, NTL>(g, e, gv[k]);
         load_v<XT, V, NTL>(x, e, xv[k]);
@@ -264,7 +303,7 @@ __global__ __launch_bounds__(B) void k_local_step(StepParams p) {
     }
 #pragma unroll
     for (int k = 0; k < U; ++k) {
-      const int64_t e = base + ((int64_t)k * B + threadIdx.x) * V;
+      const int64_t e = tile_elem<B * V * U, C>(tile, (k * B + (int)threadIdx.x) * V);
       if (e >= p.P) continue;
 #pragma unroll
       for (int t = 0; t < V; ++t) {
@@ -312,7 +351,7 @@ __device__ __forceinline__ float mean_of(float s0, double d, double rk) {
 // k_replica_mean, so both paths give bit-identical results -- then writes
 // that mean to all K rows.  The separate mean pass (2 K sizeof(T) bytes
 // per element per due state) disappears.
-template <int FORM, int N, typename XT, typename GT, int V, int NTM, int ORDER>
+template <int FORM, int N, typename XT, typename GT, int V, int NTM, int ORDER, int C = 0>
 __global__ __launch_bounds__(kBlock) void k_local_step_sync(StepParams p, uint32_t mask, int32_t K) {
   constexpr bool NTL = (NTM & 1) != 0, NTS = (NTM & 2) != 0;
   const bool sync_x = (mask & 1u) != 0;
@@ -325,7 +364,7 @@ __global__ __launch_bounds__(kBlock) void k_local_step_sync(StepParams p, uint32
   const double rk = 1.0 / (double)K;
 
   for (int64_t tile = blockIdx.x; tile < p.tiles; tile += gridDim.x) {
-    const int64_t e = tile * (int64_t)(kBlock * V) + (int64_t)threadIdx.x * V;
+    const int64_t e = tile_elem<kBlock * V, C>(tile, (int)threadIdx.x * V);
     if (e >= p.P) continue;
     float x0[V], u0[N][V], v0[V];
     double dx[V], du[N][V], dv[V];
@@ -510,7 +549,7 @@ void k_local_step_sync_waves(StepParams p, uint32_t mask, int32_t K) {
 // pass 1 updates every replica's moments and stores the ones not due (the
 // same thread reloads them in pass 2) and the means of the due ones; pass 2
 // forms each replica's direction and updates x.
-template <int N, typename XT, typename GT, int V, int NTM>
+template <int N, typename XT, typename GT, int V, int NTM, int C = 0>
 __global__ __launch_bounds__(kBlock) void k_sgdm_averaged_momenta(StepParams p, uint32_t mask, int32_t K) {
 #pragma clang fp contract(off)
   constexpr bool NTL = (NTM & 1) != 0, NTS = (NTM & 2) != 0;
@@ -523,7 +562,7 @@ __global__ __launch_bounds__(kBlock) void k_sgdm_averaged_momenta(StepParams p, 
   const double rk = 1.0 / (double)K;
 
   for (int64_t tile = blockIdx.x; tile < p.tiles; tile += gridDim.x) {
-    const int64_t e = tile * (int64_t)(kBlock * V) + (int64_t)threadIdx.x * V;
+    const int64_t e = tile_elem<kBlock * V, C>(tile, (int)threadIdx.x * V);
     if (e >= p.P) continue;
     // pass 1: u^j of every replica; due ones become their replica mean
     float u0[N][V];
@@ -647,17 +686,16 @@ struct MeanParams {
 // S^0 + (sum_{m>=1} (S^m - S^0)) / K (mean_of) and is stored to all K rows.
 // Each thread reads the K rows of its own columns and writes them back, so
 // the in-place update has no cross-thread hazard.
-template <typename T, int V, bool NT, int U = 1>
+template <typename T, int V, bool NT, int U = 1, int C = 0>
 __global__ __launch_bounds__(kBlock) void k_replica_mean(MeanParams p) {
   T* __restrict__ s = reinterpret_cast<T*>(p.state[blockIdx.y]);
   const double rk = 1.0 / (double)p.K;
   for (int64_t tile = blockIdx.x; tile < p.tiles; tile += gridDim.x) {
-    const int64_t base = tile * (int64_t)(kBlock * V * U);
     float s0[U][V];
     double d[U][V];
 #pragma unroll
     for (int k = 0; k < U; ++k) {
-      const int64_t e = base + ((int64_t)k * kBlock + threadIdx.x) * V;
+      const int64_t e = tile_elem<kBlock * V * U, C>(tile, (k * kBlock + (int)threadIdx.x) * V);
       if (e < p.P) load_v<T, V, NT>(s, e, s0[k]);
 #pragma unroll
       for (int t = 0; t < V; ++t) d[k][t] = 0.0;
@@ -666,7 +704,7 @@ __global__ __launch_bounds__(kBlock) void k_replica_mean(MeanParams p) {
     for (int32_t m = 1; m < p.K; ++m) {
 #pragma unroll
       for (int k = 0; k < U; ++k) {
-        const int64_t e = base + ((int64_t)k * kBlock + threadIdx.x) * V;
+        const int64_t e = tile_elem<kBlock * V * U, C>(tile, (k * kBlock + (int)threadIdx.x) * V);
         if (e >= p.P) continue;
         float a[V];
         load_v<T, V, NT>(s + (int64_t)m * p.P, e, a);
@@ -676,7 +714,7 @@ __global__ __launch_bounds__(kBlock) void k_replica_mean(MeanParams p) {
     }
 #pragma unroll
     for (int k = 0; k < U; ++k) {
-      const int64_t e = base + ((int64_t)k * kBlock + threadIdx.x) * V;
+      const int64_t e = tile_elem<kBlock * V * U, C>(tile, (k * kBlock + (int)threadIdx.x) * V);
       if (e >= p.P) continue;
 #pragma unroll
       for (int t = 0; t < V; ++t) s0[k][t] = mean_of(s0[k][t], d[k][t], rk);
@@ -697,23 +735,22 @@ __device__ __forceinline__ double wave_sum(double a) {
 
 // Partial sums of g^2 in fp64 for replica blockIdx.y; each block writes
 // one partial (fixed order: deterministic for a fixed grid).
-template <typename GT, int V, int U>
+template <typename GT, int V, int U, int C = 0>
 __global__ __launch_bounds__(kBlock) void k_sumsq_partial(const void* gp, int64_t P, int64_t tiles,
                                                           double* __restrict__ partials) {
   const int64_t row = (int64_t)blockIdx.y * P;
   const GT* __restrict__ g = reinterpret_cast<const GT*>(gp) + row;
   double acc = 0.0;
   for (int64_t tile = blockIdx.x; tile < tiles; tile += gridDim.x) {
-    const int64_t base = tile * (int64_t)(kBlock * V * U);
     float a[U][V];
 #pragma unroll
     for (int k = 0; k < U; ++k) {
-      const int64_t e = base + ((int64_t)k * kBlock + threadIdx.x) * V;
+      const int64_t e = tile_elem<kBlock * V * U, C>(tile, (k * kBlock + (int)threadIdx.x) * V);
       if (e < P) load_v<GT, V, false>(g, e, a[k]);
     }
 #pragma unroll
     for (int k = 0; k < U; ++k) {
-      const int64_t e = base + ((int64_t)k * kBlock + threadIdx.x) * V;
+      const int64_t e = tile_elem<kBlock * V * U, C>(tile, (k * kBlock + (int)threadIdx.x) * V);
       if (e >= P) continue;
 #pragma unroll
       for (int t = 0; t < V; ++t) {
@@ -764,7 +801,7 @@ constexpr int kStatsStride = 4 + 2 * kStatsMaxK;  // doubles per state (layout i
 // sum_m ||c^m - cbar||^2, ||xo||^2, ||c^m||^2 and <c^m, cbar>, with
 // c^m = S^m, or c^m = xo - x^m for x under a Nesterov OuterOpt.  Needs
 // K <= kStatsMaxK (every row of a column is held in registers).
-template <typename T, int V>
+template <typename T, int V, int C = 0>
 __global__ __launch_bounds__(kBlock) void k_replica_mean_stats(MeanParams p, double* __restrict__ partials) {
   T* __restrict__ s = reinterpret_cast<T*>(p.state[blockIdx.y]);
   const bool outer = (int32_t)blockIdx.y == p.outer_state && p.outer.xo != nullptr;
@@ -774,7 +811,7 @@ __global__ __launch_bounds__(kBlock) void k_replica_mean_stats(MeanParams p, dou
 #pragma unroll
   for (int m = 0; m < kStatsMaxK; ++m) a_sq[m] = a_dot[m] = 0.0;
   for (int64_t tile = blockIdx.x; tile < p.tiles; tile += gridDim.x) {
-    const int64_t e = tile * (int64_t)(kBlock * V) + (int64_t)threadIdx.x * V;
+    const int64_t e = tile_elem<kBlock * V, C>(tile, (int)threadIdx.x * V);
     if (e >= p.P) continue;
     float r[kStatsMaxK][V];
 #pragma unroll

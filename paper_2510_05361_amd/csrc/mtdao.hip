@@ -36,9 +36,13 @@ namespace {
 
 thread_local std::string g_err;
 
-// Vector slots per thread in the local step (measured on MI355X: two for
-// Adam's 6-read/5-write stream, one for SGDM and ADOPT).
-constexpr int step_slots(int form) { return form == kAdam ? 2 : 1; }
+// Vector slots per thread in the local step: one for every form (measured
+// on MI355X with 1 KiB pieces: two slots were 0-0.5 % slower for Adam's
+// 6-read/5-write stream and equal for SGDM and ADOPT).
+constexpr int step_slots(int) { return 1; }
+// Piece length of the tile -> element map (tile_elem): one wavefront's
+// access, 64 lanes of V elements (1 KiB of fp32 for V = 4).
+constexpr int piece_for(int V) { return 64 * V; }
 constexpr int kStepNT = 3;     // nontemporal hints of the local step (bit 0 loads, bit 1 stores)
 constexpr bool kMeanNT = true; // nontemporal hints of the replica mean
 constexpr int kNormU = 4;      // vector slots per thread in the norm pass
@@ -220,17 +224,18 @@ void launch_step(const mtdao_config& c, StepParams p, int V, hipStream_t st) {
     constexpr int FORM = decltype(form)::value, N = decltype(n)::value, VV = decltype(vw)::value;
     using XT = typename decltype(xt)::type;
     using GT = typename decltype(gt)::type;
-    constexpr int U = step_slots(FORM);
-    const int64_t per = (int64_t)kBlock * VV * U;
-    p.tiles = (p.P + per - 1) / per;
+    constexpr int U = step_slots(FORM), C = piece_for(VV);
+    p.tiles = tiles_for<kBlock * VV * U, C>(p.P);
     const dim3 grid = grid_for(p.tiles, c.replicas);
     if constexpr (FORM == kAdopt) {
       if (c.adopt_order == MTDAO_ADOPT_CUR) {
-        hipLaunchKernelGGL((k_local_step<FORM, N, XT, GT, VV, U, kStepNT, kCur>), grid, dim3(kBlock), 0, st, p);
+        hipLaunchKernelGGL((k_local_step<FORM, N, XT, GT, VV, U, kStepNT, kCur, kBlock, C>), grid, dim3(kBlock), 0,
+                           st, p);
         return;
       }
     }
-    hipLaunchKernelGGL((k_local_step<FORM, N, XT, GT, VV, U, kStepNT, kPrev>), grid, dim3(kBlock), 0, st, p);
+    hipLaunchKernelGGL((k_local_step<FORM, N, XT, GT, VV, U, kStepNT, kPrev, kBlock, C>), grid, dim3(kBlock), 0, st,
+                       p);
   });
 }
 
@@ -257,18 +262,18 @@ void launch_step_sync(const mtdao_config& c, StepParams p, int V, uint32_t mask,
                          c.replicas);
       return;
     }
-    const int64_t per = (int64_t)kBlock * VV;
-    p.tiles = (p.P + per - 1) / per;
+    constexpr int C = piece_for(VV);
+    p.tiles = tiles_for<kBlock * VV, C>(p.P);
     const dim3 grid = grid_for(p.tiles, 1);
     if constexpr (FORM == kAdopt) {
       if (c.adopt_order == MTDAO_ADOPT_CUR) {
-        hipLaunchKernelGGL((k_local_step_sync<FORM, N, XT, GT, VV, kStepNT, kCur>), grid, dim3(kBlock), 0, st, p, mask,
-                           c.replicas);
+        hipLaunchKernelGGL((k_local_step_sync<FORM, N, XT, GT, VV, kStepNT, kCur, C>), grid, dim3(kBlock), 0, st, p,
+                           mask, c.replicas);
         return;
       }
     }
-    hipLaunchKernelGGL((k_local_step_sync<FORM, N, XT, GT, VV, kStepNT, kPrev>), grid, dim3(kBlock), 0, st, p, mask,
-                       c.replicas);
+    hipLaunchKernelGGL((k_local_step_sync<FORM, N, XT, GT, VV, kStepNT, kPrev, C>), grid, dim3(kBlock), 0, st, p,
+                       mask, c.replicas);
   });
 }
 
@@ -286,27 +291,31 @@ void launch_adopt_init(const void* g, float* v, int64_t P, int32_t K, int V, hip
 
 template <typename GT>
 void launch_norm(const void* g, int64_t P, int32_t K, int V, int32_t nb, double* partials, hipStream_t st) {
-  const int64_t per = (int64_t)kBlock * kNormU;
   if (V == 1) {
-    hipLaunchKernelGGL((k_sumsq_partial<GT, 1, kNormU>), dim3(nb, K), dim3(kBlock), 0, st, g, P, (P + per - 1) / per,
-                       partials);
+    constexpr int C = piece_for(1);
+    hipLaunchKernelGGL((k_sumsq_partial<GT, 1, kNormU, C>), dim3(nb, K), dim3(kBlock), 0, st, g, P,
+                       tiles_for<kBlock * kNormU, C>(P), partials);
   } else {
-    hipLaunchKernelGGL((k_sumsq_partial<GT, 4, kNormU>), dim3(nb, K), dim3(kBlock), 0, st, g, P,
-                       (P + 4 * per - 1) / (4 * per), partials);
+    constexpr int C = piece_for(4);
+    hipLaunchKernelGGL((k_sumsq_partial<GT, 4, kNormU, C>), dim3(nb, K), dim3(kBlock), 0, st, g, P,
+                       tiles_for<kBlock * 4 * kNormU, C>(P), partials);
   }
 }
 
 template <typename T>
 void launch_mean(MeanParams p, int nstates, int V, hipStream_t st) {
   if (V == 1) {
-    p.tiles = (p.P + kBlock - 1) / kBlock;
-    hipLaunchKernelGGL((k_replica_mean<T, 1, kMeanNT>), grid_for(p.tiles, nstates), dim3(kBlock), 0, st, p);
+    p.tiles = tiles_for<kBlock, piece_for(1)>(p.P);
+    hipLaunchKernelGGL((k_replica_mean<T, 1, kMeanNT, 1, piece_for(1)>), grid_for(p.tiles, nstates), dim3(kBlock), 0,
+                       st, p);
   } else if (V == 4) {
-    p.tiles = (p.P + 4 * kBlock - 1) / (4 * kBlock);
-    hipLaunchKernelGGL((k_replica_mean<T, 4, kMeanNT>), grid_for(p.tiles, nstates), dim3(kBlock), 0, st, p);
+    p.tiles = tiles_for<4 * kBlock, piece_for(4)>(p.P);
+    hipLaunchKernelGGL((k_replica_mean<T, 4, kMeanNT, 1, piece_for(4)>), grid_for(p.tiles, nstates), dim3(kBlock), 0,
+                       st, p);
   } else {
-    p.tiles = (p.P + 8 * kBlock - 1) / (8 * kBlock);
-    hipLaunchKernelGGL((k_replica_mean<T, 8, kMeanNT>), grid_for(p.tiles, nstates), dim3(kBlock), 0, st, p);
+    p.tiles = tiles_for<8 * kBlock, piece_for(8)>(p.P);
+    hipLaunchKernelGGL((k_replica_mean<T, 8, kMeanNT, 1, piece_for(8)>), grid_for(p.tiles, nstates), dim3(kBlock), 0,
+                       st, p);
   }
 }
 
@@ -340,10 +349,10 @@ void launch_sgdm_averaged_momenta(const mtdao_config& c, StepParams p, int V, ui
     if constexpr (FORM == kSgdm) {
       using XT = typename decltype(xt)::type;
       using GT = typename decltype(gt)::type;
-      const int64_t per = (int64_t)kBlock * VV;
-      p.tiles = (p.P + per - 1) / per;
-      hipLaunchKernelGGL((k_sgdm_averaged_momenta<N, XT, GT, VV, kStepNT>), grid_for(p.tiles, 1), dim3(kBlock), 0, st,
-                         p, mask, c.replicas);
+      constexpr int C = piece_for(VV);
+      p.tiles = tiles_for<kBlock * VV, C>(p.P);
+      hipLaunchKernelGGL((k_sgdm_averaged_momenta<N, XT, GT, VV, kStepNT, C>), grid_for(p.tiles, 1), dim3(kBlock), 0,
+                         st, p, mask, c.replicas);
     }
   });
 }
@@ -688,9 +697,11 @@ int32_t mtdao_sync_stats(mtdao_handle* h, uint32_t mask, uint32_t* applied_mask,
   const bool fp32_vec = c.numel % 4 == 0, bf16_vec = c.numel % 4 == 0;  // 16-byte / 8-byte slots
   if (n > 0) {
     MeanParams q = mp;
-    q.tiles = fp32_vec ? (c.numel + 4 * kBlock - 1) / (4 * kBlock) : (c.numel + kBlock - 1) / kBlock;
-    if (fp32_vec) hipLaunchKernelGGL((k_replica_mean_stats<float, 4>), dim3(nb, n), dim3(kBlock), 0, st, q, partials);
-    else hipLaunchKernelGGL((k_replica_mean_stats<float, 1>), dim3(nb, n), dim3(kBlock), 0, st, q, partials);
+    q.tiles = fp32_vec ? tiles_for<4 * kBlock, piece_for(4)>(c.numel) : tiles_for<kBlock, piece_for(1)>(c.numel);
+    if (fp32_vec)
+      hipLaunchKernelGGL((k_replica_mean_stats<float, 4, piece_for(4)>), dim3(nb, n), dim3(kBlock), 0, st, q, partials);
+    else
+      hipLaunchKernelGGL((k_replica_mean_stats<float, 1, piece_for(1)>), dim3(nb, n), dim3(kBlock), 0, st, q, partials);
     hipLaunchKernelGGL(k_stats_finalize, dim3(n), dim3(64), 0, st, partials, nb, c.replicas, out);
   }
   const bool bf16_x = (m & 1u) && c.param_dtype == MTDAO_BF16;
@@ -699,10 +710,14 @@ int32_t mtdao_sync_stats(mtdao_handle* h, uint32_t mask, uint32_t* applied_mask,
     std::memset(q.state, 0, sizeof q.state);
     q.state[0] = h->x;
     q.outer_state = h->x_outer ? 0 : -1;
-    q.tiles = bf16_vec ? (c.numel + 4 * kBlock - 1) / (4 * kBlock) : (c.numel + kBlock - 1) / kBlock;
+    q.tiles = bf16_vec ? tiles_for<4 * kBlock, piece_for(4)>(c.numel) : tiles_for<kBlock, piece_for(1)>(c.numel);
     double* part_x = partials + (size_t)(2 + c.n_moments) * part_per_state;
-    if (bf16_vec) hipLaunchKernelGGL((k_replica_mean_stats<uint16_t, 4>), dim3(nb, 1), dim3(kBlock), 0, st, q, part_x);
-    else hipLaunchKernelGGL((k_replica_mean_stats<uint16_t, 1>), dim3(nb, 1), dim3(kBlock), 0, st, q, part_x);
+    if (bf16_vec)
+      hipLaunchKernelGGL((k_replica_mean_stats<uint16_t, 4, piece_for(4)>), dim3(nb, 1), dim3(kBlock), 0, st, q,
+                         part_x);
+    else
+      hipLaunchKernelGGL((k_replica_mean_stats<uint16_t, 1, piece_for(1)>), dim3(nb, 1), dim3(kBlock), 0, st, q,
+                         part_x);
     hipLaunchKernelGGL(k_stats_finalize, dim3(1), dim3(64), 0, st, part_x, nb, c.replicas, out + nslots * kStatsStride);
   }
   r = hip_check(&h->err, hipGetLastError(), "mtdao_sync_stats launch");
