@@ -153,7 +153,7 @@ class OracleConfig:
     def from_workload(cls, w, m_dtype: str = "f32", outer: str = "average", outer_lr: float = 1.0,
                       outer_momentum: float = 0.0) -> "OracleConfig":
         return cls(form=w.form, beta1=tuple(w.beta1), omega=tuple(w.omega), beta2=w.beta2,
-                   eps=w.eps, clip_rho=w.clip_rho, bias_correction=True, adopt_order=w.adopt_order,
+                   eps=w.eps, clip_rho=w.clip_rho, bias_correction=w.bias_correction, adopt_order=w.adopt_order,
                    x_dtype=w.param_dtype, g_dtype=w.grad_dtype, m_dtype=m_dtype,
                    period_x=w.period_x, period_u=tuple(w.period_u), period_v=w.period_v,
                    outer=outer, outer_lr=outer_lr, outer_momentum=outer_momentum)

@@ -165,7 +165,7 @@ def config_from_workload(w, start_step: int = 0, numel: Optional[int] = None,
     tn = [t.numel for t in w.tensors] if tensor_numel is None and numel is None else tensor_numel
     return make_config(w.form, w.replicas, w.beta1, w.omega, w.numel if numel is None else numel,
                        beta2=w.beta2, eps=w.eps, clip_rho=w.clip_rho, param_dtype=w.param_dtype,
-                       grad_dtype=w.grad_dtype, adopt_order=w.adopt_order, bias_correction=True,
+                       grad_dtype=w.grad_dtype, adopt_order=w.adopt_order, bias_correction=w.bias_correction,
                        period_x=w.period_x, period_u=w.period_u, period_v=w.period_v,
                        start_step=start_step, tensor_numel=tn, sync_order=sync_order, outer_opt=outer_opt,
                        outer_lr=outer_lr, outer_momentum=outer_momentum)

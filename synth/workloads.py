@@ -75,6 +75,7 @@ class Workload:
     x_std: float = 0.02
     seed_x: int = 0
     seed_g: int = 1000
+    bias_correction: bool = True   # Adam: u_j/(1 - beta_j^s), v/(1 - beta_2^s)
 
     @property
     def n_moments(self) -> int:

@@ -91,9 +91,19 @@ def test_edge_cases(form, edge):
 
 
 @pytest.mark.parametrize("variant", ["adopt_cur", "f32_params_bf16_grads", "bf16_params_f32_grads",
-                                     "adam_with_clip", "start_step_offset"])
+                                     "adam_with_clip", "start_step_offset", "adam_no_bias_correction",
+                                     "sgdm_clip_bf16_grads", "adopt_no_clamp"])
 def test_variants(variant):
-    if variant == "adopt_cur":
+    if variant == "adam_no_bias_correction":
+        w = synth.small_variant(synth.WORKLOADS["adam_n3_k4_p16m"], 30_000, tail=8).replace(
+            bias_correction=False, steps=40)
+    elif variant == "sgdm_clip_bf16_grads":
+        w = synth.small_variant(synth.WORKLOADS["sgdm_n2_k16_p354m_clip"], 30_000, tail=16).replace(
+            grad_dtype="bf16", replicas=5, steps=40)
+    elif variant == "adopt_no_clamp":
+        w = synth.small_variant(synth.WORKLOADS["adopt_n2_k8_p124m_bf16"], 30_000, tail=8).replace(
+            adopt_clip="off", steps=40)
+    elif variant == "adopt_cur":
         w = synth.small_variant(synth.WORKLOADS["adopt_n2_k8_p124m_bf16"], 30_000, tail=8).replace(
             adopt_order="cur", steps=40)
     elif variant == "f32_params_bf16_grads":
