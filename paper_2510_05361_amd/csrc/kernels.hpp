@@ -743,10 +743,20 @@ __global__ __launch_bounds__(kBlock) void k_sumsq_partial(const void* gp, int64_
   double acc = 0.0;
   for (int64_t tile = blockIdx.x; tile < tiles; tile += gridDim.x) {
     float a[U][V];
+    // The thread's last slot lies furthest along the row: when it is in
+    // range, all U loads are issued unconditionally, back to back, so U
+    // vector loads per lane are in flight (a guarded load per slot is
+    // waited on before the next is issued).
+    if (tile_elem<kBlock * V * U, C>(tile, ((U - 1) * kBlock + (int)threadIdx.x) * V) < P) {
 #pragma unroll
-    for (int k = 0; k < U; ++k) {
-      const int64_t e = tile_elem<kBlock * V * U, C>(tile, (k * kBlock + (int)threadIdx.x) * V);
-      if (e < P) load_v<GT, V, false>(g, e, a[k]);
+      for (int k = 0; k < U; ++k)
+        load_v<GT, V, false>(g, tile_elem<kBlock * V * U, C>(tile, (k * kBlock + (int)threadIdx.x) * V), a[k]);
+    } else {
+#pragma unroll
+      for (int k = 0; k < U; ++k) {
+        const int64_t e = tile_elem<kBlock * V * U, C>(tile, (k * kBlock + (int)threadIdx.x) * V);
+        if (e < P) load_v<GT, V, false>(g, e, a[k]);
+      }
     }
 #pragma unroll
     for (int k = 0; k < U; ++k) {
@@ -772,15 +782,37 @@ __global__ __launch_bounds__(kBlock) void k_sumsq_partial(const void* gp, int64_
   }
 }
 
-// scale[m] = min(1, rho / ||g^m||), 1 for a zero norm; one wavefront per replica.
-__global__ __launch_bounds__(64) void k_clip_finalize(const double* __restrict__ partials, int32_t nb,
-                                                      double rho, float* __restrict__ scale) {
+// scale[m] = min(1, rho / ||g^m||), 1 for a zero norm; one workgroup of
+// kFinalizeBlock threads per replica sums that replica's nb partials in a
+// fixed order (thread-strided, four independent accumulators per thread so
+// four loads are in flight, then waves in order): deterministic for a given
+// nb, and short next to the norm pass even with one partial per 4096
+// elements.
+constexpr int kFinalizeBlock = 1024;
+
+__global__ __launch_bounds__(kFinalizeBlock) void k_clip_finalize(const double* __restrict__ partials, int32_t nb,
+                                                                  double rho, float* __restrict__ scale) {
   const int32_t m = blockIdx.x;
-  double acc = 0.0;
-  for (int32_t i = threadIdx.x; i < nb; i += 64) acc += partials[(int64_t)m * nb + i];
-  acc = wave_sum(acc);
+  const double* __restrict__ q = partials + (int64_t)m * nb;
+  double a0 = 0.0, a1 = 0.0, a2 = 0.0, a3 = 0.0;
+  int32_t i = threadIdx.x;
+  for (; i + 3 * kFinalizeBlock < nb; i += 4 * kFinalizeBlock) {
+    a0 += q[i];
+    a1 += q[i + kFinalizeBlock];
+    a2 += q[i + 2 * kFinalizeBlock];
+    a3 += q[i + 3 * kFinalizeBlock];
+  }
+  for (; i < nb; i += kFinalizeBlock) a0 += q[i];
+  double acc = wave_sum((a0 + a1) + (a2 + a3));
+  __shared__ double ws[kFinalizeBlock / 64];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  if (lane == 0) ws[wave] = acc;
+  __syncthreads();
   if (threadIdx.x == 0) {
-    const double norm = __builtin_sqrt(acc);
+    double t = 0.0;
+#pragma unroll
+    for (int w = 0; w < kFinalizeBlock / 64; ++w) t += ws[w];
+    const double norm = __builtin_sqrt(t);
     double c = 1.0;
     if (norm > 0.0) {
       c = rho / norm;

@@ -45,8 +45,7 @@ constexpr int step_slots(int) { return 1; }
 constexpr int piece_for(int V) { return 64 * V; }
 constexpr int kStepNT = 3;     // nontemporal hints of the local step (bit 0 loads, bit 1 stores)
 constexpr bool kMeanNT = true; // nontemporal hints of the replica mean
-constexpr int kNormU = 4;      // vector slots per thread in the norm pass
-constexpr int kNormBlocksMax = 512;
+constexpr int kNormU = 8;      // vector slots per thread in the norm pass
 
 int32_t fail(std::string* sink, int32_t code, const char* fmt, ...) {
   char buf[512];
@@ -150,18 +149,23 @@ uint32_t valid_bits(const mtdao_config& c) {
   return (nb >= 32) ? 0xFFFFFFFFu : ((1u << nb) - 1u);
 }
 
-int32_t norm_blocks_for(int64_t P, int V) {
-  const int64_t per_block = (int64_t)kBlock * V * kNormU;
-  int64_t nb = (P + per_block - 1) / per_block;
-  if (nb < 1) nb = 1;
-  if (nb > kNormBlocksMax) nb = kNormBlocksMax;
-  return (int32_t)nb;
+// Workgroups per replica of the norm pass: one tile of kBlock * V * kNormU
+// elements each, so the grid (tiles, K) is dispatched replica by replica
+// and the pass streams one row at a time, like a plain read.  (A fixed
+// grid of a few hundred looping workgroups per replica keeps every row in
+// flight at once: 16 concurrent read streams at K = 16.)  One fp64 partial
+// per workgroup; P <= 2^40 keeps the count below 2^31.
+int32_t norm_blocks_for(int64_t P) {
+  const int V = (P % 4 == 0) ? 4 : 1;
+  const int64_t nb = V == 4 ? tiles_for<kBlock * 4 * kNormU, piece_for(4)>(P)
+                            : tiles_for<kBlock * kNormU, piece_for(1)>(P);
+  return (int32_t)(nb < 1 ? 1 : nb);
 }
 
 size_t workspace_for(const mtdao_config& c) {
   if (!(c.clip_rho > 0.0f) || c.form == MTDAO_ADOPT) return 0;
   const size_t scale_bytes = ((size_t)c.replicas * sizeof(float) + 255) / 256 * 256;
-  return scale_bytes + (size_t)c.replicas * kNormBlocksMax * sizeof(double);
+  return scale_bytes + (size_t)c.replicas * (size_t)norm_blocks_for(c.numel) * sizeof(double);
 }
 
 // Non-overlap of two [lo, lo + bytes) device ranges.
@@ -449,7 +453,7 @@ int32_t mtdao_init(const mtdao_config* cfg, const mtdao_buffers* bufs, void* wor
     const size_t scale_bytes = ((size_t)c.replicas * sizeof(float) + 255) / 256 * 256;
     h->scale = reinterpret_cast<float*>(workspace);
     h->partials = reinterpret_cast<double*>(reinterpret_cast<char*>(workspace) + scale_bytes);
-    h->norm_blocks = norm_blocks_for(c.numel, (c.numel % 4 == 0) ? 4 : 1);
+    h->norm_blocks = norm_blocks_for(c.numel);
   }
 
   hipStream_t st = reinterpret_cast<hipStream_t>(hip_stream);
@@ -562,7 +566,7 @@ StepParams prepare_step(mtdao_handle* h, const void* grads, float lr, float adop
     const int Vg = (P % 4 == 0) ? 4 : 1;  // 16-byte (fp32) or 8-byte (bf16) slots
     if (c.grad_dtype == MTDAO_F32) launch_norm<float>(grads, P, c.replicas, Vg, h->norm_blocks, h->partials, st);
     else launch_norm<uint16_t>(grads, P, c.replicas, Vg, h->norm_blocks, h->partials, st);
-    hipLaunchKernelGGL(k_clip_finalize, dim3(c.replicas), dim3(64), 0, st, h->partials, h->norm_blocks,
+    hipLaunchKernelGGL(k_clip_finalize, dim3(c.replicas), dim3(kFinalizeBlock), 0, st, h->partials, h->norm_blocks,
                        (double)c.clip_rho, h->scale);
     p.scale = h->scale;
   }
