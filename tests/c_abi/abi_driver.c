@@ -1,0 +1,240 @@
+/*
+ * Plain-C consumer of the MT-DAO C ABI (include/mtdao.h): no Python, no
+ * torch.  Device memory comes from hipMalloc, work goes on a HIP stream the
+ * program creates, and every state read back through mtdao_read_state is
+ * compared with the CPU oracle (oracle/_liboracle.so, test infrastructure)
+ * run on the same inputs:
+ *   case 1: Adam form (Algorithm 1), N = 3, K = 4 workers, P = 10007 (a
+ *           row length that is not a multiple of 4: the scalar path), with
+ *           every averaging event folded into mtdao_step_sync;
+ *   case 2: SGDM form (Algorithm 3), N = 2, K = 5, P = 8204, per-worker
+ *           global-norm clip rho = 0.05 (active), mtdao_local_step followed
+ *           by mtdao_sync on the schedule.
+ * Inputs are seeded splitmix64 fields made here; the driver holds none of
+ * the method's arithmetic.  Pass: every applied mask equals the oracle's
+ * schedule bit for bit, and every state's max |a - b| / max(|b|, rms(b))
+ * is at most 1e-5.  Prints one line per case; exit status 0 on success.
+ */
+#include <hip/hip_runtime_api.h>
+#include <math.h>
+#include <stdint.h>
+#include <stdio.h>
+#include <stdlib.h>
+#include <string.h>
+
+#include "mtdao.h"
+
+/* ---- the oracle's C interface (oracle/mtdao_oracle.c) ---- */
+typedef struct {
+  int32_t form, n, x_dtype, g_dtype, m_dtype, bias_correction, adopt_order;
+  float beta1[4], omega[4], beta2, eps;
+} oracle_cfg;
+uint32_t oracle_schedule(int64_t s, int32_t n, int32_t period_x, const int32_t* period_u, int32_t period_v,
+                         int32_t has_v);
+double oracle_sumsq(const void* g, int32_t g_dtype, int64_t n);
+double oracle_clip_scale(double norm, double rho);
+void oracle_local_step(const oracle_cfg* c, int64_t s, float lr, float clip_c, const double* scale, void* x,
+                       void* const* u, void* v, const void* g, int64_t K, int64_t P);
+void oracle_replica_mean(void* state, int32_t dtype, int64_t K, int64_t P);
+
+#define CHECK_HIP(call)                                                              \
+  do {                                                                               \
+    hipError_t e_ = (call);                                                          \
+    if (e_ != hipSuccess) {                                                          \
+      fprintf(stderr, "%s:%d %s: %s\n", __FILE__, __LINE__, #call, hipGetErrorString(e_)); \
+      exit(2);                                                                       \
+    }                                                                                \
+  } while (0)
+#define CHECK_MT(h, call)                                                            \
+  do {                                                                               \
+    int32_t r_ = (call);                                                             \
+    if (r_ != MTDAO_OK) {                                                            \
+      fprintf(stderr, "%s:%d %s = %d: %s\n", __FILE__, __LINE__, #call, r_, mtdao_last_error(h)); \
+      exit(3);                                                                       \
+    }                                                                                \
+  } while (0)
+
+/* seeded inputs: splitmix64 -> uniform in [-1, 1) */
+static uint64_t mix(uint64_t z) {
+  z += 0x9E3779B97F4A7C15ull;
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
+}
+static float field(uint64_t seed, int64_t i) {
+  return (float)((double)(mix(seed * 0x100000001B3ull + (uint64_t)i) >> 11) * 0x1p-52 - 1.0);
+}
+
+typedef struct {
+  const char* name;
+  int32_t form, K, N;
+  int64_t P;
+  float beta1[4], omega[4], beta2, eps, rho, lr;
+  int32_t period_x, period_u[4], period_v, steps, fused;
+} drv_case;
+
+static double compare(const float* a, const float* b, int64_t n) {
+  double ss = 0.0, worst = 0.0;
+  for (int64_t i = 0; i < n; ++i) ss += (double)b[i] * (double)b[i];
+  const double rms = sqrt(ss / (double)(n > 0 ? n : 1));
+  for (int64_t i = 0; i < n; ++i) {
+    const double den = fmax(fabs((double)b[i]), rms);
+    const double d = den > 0.0 ? fabs((double)a[i] - (double)b[i]) / den : fabs((double)a[i] - (double)b[i]);
+    if (!(d <= worst)) worst = d; /* NaN propagates as a failure */
+  }
+  return worst;
+}
+
+static int run_case(const drv_case* t) {
+  const int32_t K = t->K, N = t->N;
+  const int64_t P = t->P, KP = (int64_t)K * P;
+  const int has_v = t->form != MTDAO_SGDM;
+  hipStream_t st;
+  CHECK_HIP(hipStreamCreate(&st));
+
+  mtdao_config c;
+  memset(&c, 0, sizeof c);
+  c.form = t->form;
+  c.replicas = K;
+  c.n_moments = N;
+  c.param_dtype = MTDAO_F32;
+  c.grad_dtype = MTDAO_F32;
+  c.adopt_order = MTDAO_ADOPT_PREV;
+  c.bias_correction = t->form == MTDAO_ADAM;
+  for (int j = 0; j < N; ++j) {
+    c.beta1[j] = t->beta1[j];
+    c.omega[j] = t->omega[j];
+    c.period_u[j] = t->period_u[j];
+  }
+  c.beta2 = t->beta2;
+  c.eps = t->eps;
+  c.clip_rho = t->rho;
+  c.period_x = t->period_x;
+  c.period_v = t->period_v;
+  c.numel = P;
+  c.sync_order = MTDAO_SYNC_AFTER_STEP;
+  c.outer_opt = MTDAO_OUTER_AVERAGE;
+
+  /* device buffers */
+  void* dx;
+  float* du[MTDAO_MAX_N] = {0};
+  float* dv = NULL;
+  float* dg;
+  void* ws = NULL;
+  CHECK_HIP(hipMalloc(&dx, (size_t)KP * 4));
+  for (int j = 0; j < N; ++j) CHECK_HIP(hipMalloc((void**)&du[j], (size_t)KP * 4));
+  if (has_v) CHECK_HIP(hipMalloc((void**)&dv, (size_t)KP * 4));
+  CHECK_HIP(hipMalloc((void**)&dg, (size_t)KP * 4));
+  size_t ws_bytes = 0;
+  CHECK_MT(NULL, mtdao_workspace_bytes(&c, &ws_bytes));
+  if (ws_bytes) CHECK_HIP(hipMalloc(&ws, ws_bytes));
+
+  /* host oracle states and the inputs */
+  float* x = malloc((size_t)KP * 4);
+  float* u[MTDAO_MAX_N] = {0};
+  for (int j = 0; j < N; ++j) u[j] = calloc((size_t)KP, 4);
+  float* v = has_v ? calloc((size_t)KP, 4) : NULL;
+  float* g = malloc((size_t)KP * 4);
+  float* back = malloc((size_t)KP * 4);
+  for (int64_t i = 0; i < P; ++i) x[i] = 0.02f * field(7, i);
+  for (int32_t m = 1; m < K; ++m) memcpy(x + (int64_t)m * P, x, (size_t)P * 4);
+  CHECK_HIP(hipMemcpy(dx, x, (size_t)P * 4, hipMemcpyHostToDevice)); /* row 0: x_0, broadcast by init */
+
+  mtdao_buffers b;
+  memset(&b, 0, sizeof b);
+  b.x = dx;
+  for (int j = 0; j < N; ++j) b.u[j] = du[j];
+  b.v = dv;
+  b.init_states = 0;
+  mtdao_handle* h = NULL;
+  CHECK_MT(NULL, mtdao_init(&c, &b, ws, ws_bytes, (void*)st, &h));
+
+  oracle_cfg oc;
+  memset(&oc, 0, sizeof oc);
+  oc.form = t->form;
+  oc.n = N;
+  oc.x_dtype = oc.g_dtype = oc.m_dtype = 0; /* fp32 storage */
+  oc.bias_correction = c.bias_correction;
+  oc.adopt_order = 0;
+  for (int j = 0; j < N; ++j) {
+    oc.beta1[j] = t->beta1[j];
+    oc.omega[j] = t->omega[j];
+  }
+  oc.beta2 = t->beta2;
+  oc.eps = t->eps;
+  void* ou[MTDAO_MAX_N];
+  for (int j = 0; j < N; ++j) ou[j] = u[j];
+  double scale[64];
+  int masks_ok = 1;
+  uint32_t nsync = 0;
+
+  for (int32_t s = 1; s <= t->steps; ++s) {
+    for (int32_t m = 0; m < K; ++m)
+      for (int64_t i = 0; i < P; ++i) g[(int64_t)m * P + i] = 1e-2f * field(1000 + 131 * (uint64_t)s + m, i);
+    CHECK_HIP(hipMemcpyAsync(dg, g, (size_t)KP * 4, hipMemcpyHostToDevice, st));
+    uint32_t applied = 0;
+    if (t->fused) {
+      CHECK_MT(h, mtdao_step_sync(h, dg, t->lr, 0.0f, MTDAO_SYNC_AUTO, &applied, (void*)st));
+    } else {
+      CHECK_MT(h, mtdao_local_step(h, dg, t->lr, 0.0f, (void*)st));
+      CHECK_MT(h, mtdao_sync(h, MTDAO_SYNC_AUTO, &applied, (void*)st));
+    }
+    /* the oracle: clip factors, the step, then the schedule's means */
+    for (int32_t m = 0; m < K; ++m)
+      scale[m] = oracle_clip_scale(sqrt(oracle_sumsq(g + (int64_t)m * P, 0, P)), (double)t->rho);
+    oracle_local_step(&oc, s, t->lr, 0.0f, t->rho > 0.0f ? scale : NULL, x, ou, v, g, K, P);
+    const uint32_t want = oracle_schedule(s, N, t->period_x, t->period_u, t->period_v, has_v);
+    if (want & 1u) oracle_replica_mean(x, 0, K, P);
+    for (int j = 0; j < N; ++j)
+      if (want & (1u << (j + 1))) oracle_replica_mean(u[j], 0, K, P);
+    if (has_v && (want & (1u << (N + 1)))) oracle_replica_mean(v, 0, K, P);
+    if (applied != want) {
+      fprintf(stderr, "%s: step %d applied mask 0x%x, oracle 0x%x\n", t->name, s, applied, want);
+      masks_ok = 0;
+    }
+    nsync += (uint32_t)__builtin_popcount(want);
+    CHECK_HIP(hipStreamSynchronize(st)); /* g is rewritten next step */
+  }
+
+  /* every state of every worker, read back through the ABI */
+  const int nstates = 1 + N + (has_v ? 1 : 0);
+  double worst = 0.0;
+  for (int sid = 0; sid < nstates; ++sid) {
+    const float* ref = sid == 0 ? x : (sid <= N ? u[sid - 1] : v);
+    for (int32_t m = 0; m < K; ++m)
+      CHECK_MT(h, mtdao_read_state(h, sid, m, 0, P, back + (int64_t)m * P, (void*)st));
+    const double e = compare(back, ref, KP);
+    if (!(e <= worst)) worst = e;
+  }
+  const int64_t count = mtdao_step_count(h);
+  mtdao_destroy(h);
+  const int ok = masks_ok && worst <= 1e-5 && count == t->steps;
+  printf("%s: K=%d P=%lld N=%d steps=%d state-syncs=%u max rel err %.3e masks %s -> %s\n", t->name, K,
+         (long long)P, N, t->steps, nsync, worst, masks_ok ? "match" : "DIFFER", ok ? "ok" : "FAIL");
+  fflush(stdout);
+
+  CHECK_HIP(hipFree(dx));
+  for (int j = 0; j < N; ++j) CHECK_HIP(hipFree(du[j]));
+  if (dv) CHECK_HIP(hipFree(dv));
+  CHECK_HIP(hipFree(dg));
+  if (ws) CHECK_HIP(hipFree(ws));
+  CHECK_HIP(hipStreamDestroy(st));
+  free(x);
+  for (int j = 0; j < N; ++j) free(u[j]);
+  free(v);
+  free(g);
+  free(back);
+  return ok;
+}
+
+int main(void) {
+  const drv_case cases[2] = {
+      {"adam_n3_k4_step_sync", MTDAO_ADAM, 4, 3, 10007, {0.9f, 0.99f, 0.999f}, {0.3f, 0.3f, 0.3f}, 0.999f, 1e-8f,
+       0.0f, 1e-3f, 4, {8, 8, 16}, 16, 32, 1},
+      {"sgdm_n2_k5_clip_sync", MTDAO_SGDM, 5, 2, 8204, {0.9f, 0.99f}, {0.3f, 0.6f}, 0.0f, 0.0f, 0.05f, 1e-2f, 4,
+       {2, 8}, 0, 24, 0},
+  };
+  int all = 1;
+  for (int i = 0; i < 2; ++i) all &= run_case(&cases[i]);
+  return all ? 0 : 1;
+}
