@@ -13,8 +13,10 @@ each u^j: 2, v: 1).
 
 Prints ONE JSON line.  Extra objects:
   step / sync       element-updates/s and GB/s of each part, % of HBM peak
-                    (sync: the standalone averaging pass per state, untimed
-                    region; step_sync_fused: the fused launches of the window)
+                    (step: mean and median of the timed launches with nothing
+                    due; sync: the standalone averaging pass per state, median
+                    of 20 launches outside the timed region; step_sync_fused:
+                    the fused launches of the window)
   roofline          dominant kernel (the local step): algorithmic bytes per
                     launch / mean launch time from HIP events on its stream
   cpu_baseline      the CPU oracle, unchanged, on a bounded sample of the same
@@ -77,6 +79,12 @@ def stream_lib():
     L.stream_ref_fill.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p]
     L.stream_ref_fill.restype = ctypes.c_int32
     return L
+
+
+def _median(xs):
+    ys = sorted(xs)
+    n = len(ys)
+    return ys[n // 2] if n % 2 else 0.5 * (ys[n // 2 - 1] + ys[n // 2])
 
 
 def achievable(nbytes: int = 8 << 30, reps: int = 5):
@@ -317,19 +325,19 @@ def main() -> int:
     # the dominant kernel: the local step on steps with nothing due
     step_launch_s = (sum(plain) / len(plain) if plain else sum(call_ms) / len(call_ms)) / 1e3
 
-    # per-state sync time (replica mean of one state), untimed region
+    # per-state sync time (replica mean of one state), untimed region: the
+    # median of 20 launches, each bracketed by its own events
     nstates = 1 + w.n_moments + (1 if w.has_v else 0)
     sync_s = []
     for sid in range(nstates):
-        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         opt.sync(1 << sid)
-        a.record(stream)
-        reps = 5
-        for _ in range(reps):
+        sev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(20)]
+        for a, b in sev:
+            a.record(stream)
             opt.sync(1 << sid)
-        b.record(stream)
+            b.record(stream)
         torch.cuda.synchronize()
-        sync_s.append(a.elapsed_time(b) / reps / 1e3)
+        sync_s.append(_median([a.elapsed_time(b) for a, b in sev]) / 1e3)
     opt.close()
     del opt, grads
     torch.cuda.empty_cache()
@@ -368,7 +376,9 @@ def main() -> int:
                    "n_moments": w.n_moments, "param_dtype": w.param_dtype, "grad_dtype": w.grad_dtype,
                    "periods": {"x": w.period_x, "u": list(w.period_u), "v": w.period_v},
                    "syncs_in_window": {str(k): v for k, v in sorted(syncs.items())}},
-        "step": {"mean_launch_ms": step_launch_s * 1e3, "element_updates_per_s": K * P / step_launch_s,
+        "step": {"mean_launch_ms": step_launch_s * 1e3,
+                 "median_launch_ms": _median(plain if plain else call_ms),
+                 "element_updates_per_s": K * P / step_launch_s,
                  "bytes_per_element_update": eb, "GBps": step_gbs,
                  "pct_hbm_peak": 100 * step_gbs / HBM_PEAK_GBS,
                  "pct_of_plain_copy": 100 * step_gbs / ceil["copy_GBps"]},
