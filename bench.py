@@ -248,6 +248,116 @@ def calibrate_copy(nbytes: int, reps: int) -> None:
                       "GBps_read_plus_write": 2 * n4 * 16 / dt / 1e9}), flush=True)
 
 
+def _time_calls(fn, reps: int, stream) -> float:
+    """Mean seconds per call of fn (enqueues on ``stream``), HIP events
+    around each call; one untimed call first."""
+    import torch
+
+    fn()
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+    for a, b in evs:
+        a.record(stream)
+        fn()
+        b.record(stream)
+    torch.cuda.synchronize()
+    return sum(a.elapsed_time(b) for a, b in evs) / reps / 1e3
+
+
+def _part(name: str, seconds: float, nbytes: float, kernel: str, copy_gbs: float) -> dict:
+    gbs = nbytes / seconds / 1e9
+    return {"part": name, "kernel": kernel, "mean_launch_ms": seconds * 1e3, "algorithmic_bytes": nbytes,
+            "GBps": gbs, "pct_hbm_peak": 100 * gbs / HBM_PEAK_GBS, "pct_of_plain_copy": 100 * gbs / copy_gbs}
+
+
+def measure_row(args) -> int:
+    """Launch time and bandwidth of the kernels behind one of the paths
+    beyond the plain step, at full size (one JSON line):
+      outer  Nesterov OuterOpt at an x averaging event: the standalone mean
+             of x with the outer step, and the fused step + x mean + outer
+             step (bench workload, outer lr 0.7, momentum 0.9)
+      stats  mtdao_sync_stats of every state (bench workload): the mean
+             plus the averaging diagnostics, one call, host wait included
+      prob   Algorithm 4's step with averaged momenta (SGDM, K = 16,
+             beta = (0, 0.99), omega = (0.3, 0.7), no clip): every momentum
+             due, and momenta and x due
+    Each part is reported against its algorithmic bytes and next to the
+    plain local step of the same buffers."""
+    import torch
+
+    import synth
+    from paper_2510_05361_amd import mtdao as abi
+    from paper_2510_05361_amd.optimizer import MtdaoOptimizer
+    from synth.device import DeviceInputs
+
+    d = torch.device("cuda:0")
+    if args.row == "prob":
+        w = synth.WORKLOADS["sgdm_n2_k16_p354m_clip"].replace(beta1=(0.0, 0.99), omega=(0.3, 0.7), clip_rho=0.0,
+                                                              period_x=0, period_u=(0, 0))
+        cfg = abi.config_from_workload(w, sync_order=abi.MTDAO_SYNC_MOMENTA_IN_STEP)
+    elif args.row == "outer":
+        w = synth.WORKLOADS[args.workload]
+        cfg = abi.config_from_workload(w, outer_opt=abi.MTDAO_OUTER_NESTEROV, outer_lr=0.7, outer_momentum=0.9)
+    else:
+        w = synth.WORKLOADS[args.workload]
+        cfg = abi.config_from_workload(w)
+    K, P = w.replicas, w.numel
+    print(f"bench --row {args.row}: {w.name} K={K} P={P}", file=sys.stderr, flush=True)
+    dev = DeviceInputs(w, d)
+    opt = MtdaoOptimizer(cfg, d, x0=dev.x0_row())
+    gdt = torch.bfloat16 if w.grad_dtype == "bf16" else torch.float32
+    grads = torch.empty((K, P), dtype=gdt, device=d)
+    dev.grads_into(1, grads)
+    del dev
+    torch.cuda.synchronize()
+    st = torch.cuda.current_stream()
+    reps = max(1, args.steps)
+    xs = 2 if w.param_dtype == "bf16" else 4
+    eb = step_bytes_per_element(w)
+    step_bytes = K * P * eb
+    mean_bytes = [2 * K * xs * P] + [2 * K * 4 * P] * (w.n_moments + (1 if w.has_v else 0))
+    for _ in range(args.warmup):
+        opt.step_sync(grads, w.lr, w.adopt_clip_value(2), 0)
+    plain_s = _time_calls(lambda: opt.step_sync(grads, w.lr, w.adopt_clip_value(2), 0), reps, st)
+    parts = []
+    if args.row == "outer":
+        mean_s = _time_calls(lambda: opt.sync(1), reps, st)
+        fused_s = _time_calls(lambda: opt.step_sync(grads, w.lr, w.adopt_clip_value(2), 1), reps, st)
+        ceil = achievable()
+        parts.append(_part("mean of x + outer step", mean_s, mean_bytes[0] + 16 * P,
+                           "k_replica_mean_waves (outer epilogue)", ceil["copy_GBps"]))
+        parts.append(_part("fused step + mean of x + outer step", fused_s, step_bytes + 16 * P,
+                           "k_local_step_sync_waves (outer epilogue)", ceil["copy_GBps"]))
+    elif args.row == "stats":
+        nst = len(mean_bytes)
+        per_state = [_time_calls(lambda sid=sid: opt.sync_stats(1 << sid), reps, st) for sid in range(nst)]
+        all_s = _time_calls(lambda: opt.sync_stats((1 << nst) - 1), reps, st)
+        plain_mean = [_time_calls(lambda sid=sid: opt.sync(1 << sid), reps, st) for sid in range(nst)]
+        ceil = achievable()
+        for sid in range(nst):
+            parts.append(_part(f"sync_stats state {sid}", per_state[sid], mean_bytes[sid],
+                               "k_replica_mean_stats + k_stats_finalize + copy to host", ceil["copy_GBps"]))
+            parts.append(_part(f"plain mean state {sid}", plain_mean[sid], mean_bytes[sid],
+                               "k_replica_mean_waves", ceil["copy_GBps"]))
+        parts.append(_part("sync_stats all states, one call", all_s, sum(mean_bytes),
+                           "k_replica_mean_stats (fp32 states) + k_stats_finalize + copy to host", ceil["copy_GBps"]))
+    else:
+        mom = ((1 << w.n_moments) - 1) << 1
+        prob_u_s = _time_calls(lambda: opt.step_sync(grads, w.lr, 0.0, mom), reps, st)
+        prob_all_s = _time_calls(lambda: opt.step_sync(grads, w.lr, 0.0, mom | 1), reps, st)
+        ceil = achievable()
+        parts.append(_part("step with every momentum averaged in the step", prob_u_s, step_bytes,
+                           "k_sgdm_averaged_momenta", ceil["copy_GBps"]))
+        parts.append(_part("step with momenta and x averaged", prob_all_s, step_bytes,
+                           "k_sgdm_averaged_momenta", ceil["copy_GBps"]))
+    opt.close()
+    out = {"row": args.row, "workload": w.name, "replicas": K, "params_per_replica": P, "form": w.form,
+           "reps": reps, "plain_step": _part("plain local step, same buffers", plain_s, step_bytes, "k_local_step",
+                                             ceil["copy_GBps"]),
+           "parts": parts, "achievable": ceil, "peak_GBps": HBM_PEAK_GBS}
+    print(json.dumps(out), flush=True)
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -255,6 +365,9 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=8)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--row", choices=["step", "outer", "stats", "prob"], default="step",
+                    help="step: the hot path (the default line); outer / stats / prob: the kernels of the "
+                         "Nesterov OuterOpt, the averaging diagnostics, Algorithm 4's step (--steps = reps)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES",
                     help="only run a plain copy of BYTES each way (counter calibration)")
     args = ap.parse_args()
@@ -267,6 +380,8 @@ def main() -> int:
     if args.calibrate_copy:
         calibrate_copy(args.calibrate_copy, max(1, args.steps))
         return 0
+    if args.row != "step":
+        return measure_row(args)
 
     import torch
 

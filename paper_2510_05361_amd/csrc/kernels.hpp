@@ -193,6 +193,25 @@ __device__ __forceinline__ void outer_step(const OuterParams& o, int64_t e, floa
   store_v<float, V, false>(o.mom, e, b);
 }
 
+// The OuterOpt over one piece of 64 V elements whose means sit in LDS,
+// means[t * 64 + l] = element l V + t of the piece starting at element e0
+// (the layout of the wave-per-replica kernels).  Wave m of the K takes
+// every K-th run of 64 consecutive elements, so the fp32 outer parameters
+// and momentum are read and written in accesses that are contiguous across
+// the lanes of a wave (the column-by-wave order of the mean phase would
+// put them 16 bytes apart).  Each element gets exactly outer_step's update.
+template <int V>
+__device__ __forceinline__ void outer_step_piece(const OuterParams& o, int64_t e0, int64_t P, int32_t K, int32_t m,
+                                                 int32_t lane, float* means) {
+  for (int j = m * 64 + lane; j < 64 * V; j += 64 * K) {
+    if (e0 + j >= P) continue;
+    const int l = j / V, t = j % V;
+    float a[1] = {means[t * 64 + l]};
+    outer_step<1>(o, e0 + j, a);
+    means[t * 64 + l] = a[0];
+  }
+}
+
 // ------------------------------------------------------------ local step
 
 // Per-launch scalars, prepared on the host in double and rounded to fp32.
@@ -524,11 +543,13 @@ void k_local_step_sync_waves(StepParams p, uint32_t mask, int32_t K) {
         double d = 0.0;
 #pragma unroll 4
         for (int32_t q = 1; q < K; ++q) mean_add(d, lds[q][t * 64 + lane], s0);
-        float mean[1] = {mean_of(s0, d, rk)};
-        if (k == 0) outer_step<1>(p.outer, e + t, mean);
-        lds[0][t * 64 + lane] = mean[0];
+        lds[0][t * 64 + lane] = mean_of(s0, d, rk);
       }
       __syncthreads();
+      if (k == 0 && p.outer.xo != nullptr) {
+        outer_step_piece<V>(p.outer, tile * (int64_t)(64 * V), p.P, K, m, lane, &lds[0][0]);
+        __syncthreads();
+      }
       if (in) {
         float mean[V];
 #pragma unroll
@@ -759,11 +780,13 @@ __global__ __launch_bounds__(64 * kWaveMaxK) void k_replica_mean_waves(MeanParam
       const float s0 = lds_mean[t * 64 + lane];
       double d = 0.0;
       for (int32_t q = 1; q < K; ++q) mean_add(d, lds_mean[(q * V + t) * 64 + lane], s0);
-      float mean[1] = {mean_of(s0, d, rk)};
-      if (outer) outer_step<1>(p.outer, e + t, mean);
-      lds_mean[t * 64 + lane] = mean[0];
+      lds_mean[t * 64 + lane] = mean_of(s0, d, rk);
     }
     __syncthreads();
+    if (outer) {
+      outer_step_piece<V>(p.outer, tile * (int64_t)(64 * V), p.P, K, m, lane, lds_mean);
+      __syncthreads();
+    }
     if (in) {
 #pragma unroll
       for (int t = 0; t < V; ++t) a[t] = lds_mean[t * 64 + lane];
