@@ -898,91 +898,139 @@ __global__ __launch_bounds__(kFinalizeBlock) void k_clip_finalize(const double* 
 constexpr int kStatsMaxK = 16;
 constexpr int kStatsStride = 4 + 2 * kStatsMaxK;  // doubles per state (layout in mtdao.h)
 
-// The replica mean of k_replica_mean (same arithmetic, same order, same
-// results) plus, from the values before averaging, per block partial sums
-// of the averaging diagnostics of state blockIdx.y: ||cbar||^2,
+// The replica mean of the wave-per-replica kernel (same pieces, same
+// mean_add / mean_of order, same values) plus, from the values before
+// averaging, the averaging diagnostics of state blockIdx.y: ||cbar||^2,
 // sum_m ||c^m - cbar||^2, ||xo||^2, ||c^m||^2 and <c^m, cbar>, with
-// c^m = S^m, or c^m = xo - x^m for x under a Nesterov OuterOpt.  Needs
-// K <= kStatsMaxK (every row of a column is held in registers).
-template <typename T, int V, int C = 0>
-__global__ __launch_bounds__(kBlock) void k_replica_mean_stats(MeanParams p, double* __restrict__ partials) {
+// c^m = S^m, or c^m = xo - x^m for x under a Nesterov OuterOpt.
+// blockDim = 64 K (1 <= K <= kStatsMaxK), dynamic LDS of K * 64 * V
+// floats; a fixed grid of workgroups walks the pieces, each wave keeping
+// fp64 sums for its own replica (wave 0 also those of cbar and xo), and
+// every workgroup writes one partial of each of the kStatsStride sums
+// (partials[state][stat][workgroup]), reduced in a fixed order:
+// deterministic for a given grid.
+template <typename T, int V>
+__global__ __launch_bounds__(64 * kStatsMaxK) void k_replica_mean_stats(MeanParams p, double* __restrict__ partials) {
+  extern __shared__ float lds_stats[];  // [K][64 V]
+  __shared__ double red[kStatsMaxK][5];
   T* __restrict__ s = reinterpret_cast<T*>(p.state[blockIdx.y]);
+  const int32_t K = p.K, m = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const bool outer = (int32_t)blockIdx.y == p.outer_state && p.outer.xo != nullptr;
-  const int32_t K = p.K;
   const double rk = 1.0 / (double)K;
-  double a_mean = 0.0, a_var = 0.0, a_ref = 0.0, a_sq[kStatsMaxK], a_dot[kStatsMaxK];
-#pragma unroll
-  for (int m = 0; m < kStatsMaxK; ++m) a_sq[m] = a_dot[m] = 0.0;
-  for (int64_t tile = blockIdx.x; tile < p.tiles; tile += gridDim.x) {
-    const int64_t e = tile_elem<kBlock * V, C>(tile, (int)threadIdx.x * V);
-    if (e >= p.P) continue;
-    float r[kStatsMaxK][V];
-#pragma unroll
-    for (int m = 0; m < kStatsMaxK; ++m)
-      if (m < K) load_v<T, V, true>(s + (int64_t)m * p.P, e, r[m]);
-    float mean[V], xo[V];
-#pragma unroll
-    for (int t = 0; t < V; ++t) {
-      double d = 0.0;
-#pragma unroll
-      for (int m = 1; m < kStatsMaxK; ++m)
-        if (m < K) mean_add(d, r[m][t], r[0][t]);
-      mean[t] = mean_of(r[0][t], d, rk);
+  T* __restrict__ row = s + (int64_t)m * p.P;
+  double a_sq = 0.0, a_dot = 0.0, a_var = 0.0, a_mean = 0.0, a_ref = 0.0;
+  // the loads of the next piece are issued before the current one is
+  // averaged and reduced, so each wave keeps a piece in flight through the
+  // barriers of the current one
+  float na[V], nxo[V];
+  {
+    const int64_t e = (int64_t)blockIdx.x * (64 * V) + (int64_t)lane * V;
+    if (blockIdx.x < p.tiles && e < p.P) {
+      load_v<T, V, true>(row, e, na);
+      if (outer) load_v<float, V, false>(p.outer.xo, e, nxo);
     }
-    if (outer) load_v<float, V, false>(p.outer.xo, e, xo);
+  }
+  for (int64_t tile = blockIdx.x; tile < p.tiles; tile += gridDim.x) {
+    const int64_t e = tile * (int64_t)(64 * V) + (int64_t)lane * V;
+    const bool in = e < p.P;
+    float a[V], xo[V];
 #pragma unroll
     for (int t = 0; t < V; ++t) {
-      const double cbar = outer ? (double)xo[t] - (double)mean[t] : (double)mean[t];
-      a_mean += cbar * cbar;
-      if (outer) a_ref += (double)xo[t] * (double)xo[t];
+      a[t] = in ? na[t] : 0.0f;
+      xo[t] = (in && outer) ? nxo[t] : 0.0f;
+    }
+    const int64_t en = e + (int64_t)gridDim.x * (64 * V);
+    if (tile + gridDim.x < p.tiles && en < p.P) {
+      load_v<T, V, true>(row, en, na);
+      if (outer) load_v<float, V, false>(p.outer.xo, en, nxo);
+    }
 #pragma unroll
-      for (int m = 0; m < kStatsMaxK; ++m) {
-        if (m >= K) continue;
-        const double c = outer ? (double)xo[t] - (double)r[m][t] : (double)r[m][t];
+    for (int t = 0; t < V; ++t) lds_stats[(m * V + t) * 64 + lane] = a[t];
+    __syncthreads();
+    for (int t = m; in && t < V; t += K) {
+      const float s0 = lds_stats[t * 64 + lane];
+      double d = 0.0;
+      for (int32_t q = 1; q < K; ++q) mean_add(d, lds_stats[(q * V + t) * 64 + lane], s0);
+      lds_stats[t * 64 + lane] = mean_of(s0, d, rk);
+    }
+    __syncthreads();
+    float mean[V];
+#pragma unroll
+    for (int t = 0; t < V; ++t) mean[t] = lds_stats[t * 64 + lane];
+    if (outer) {
+      __syncthreads();  // every wave has read the means before the outer step rewrites them
+      outer_step_piece<V>(p.outer, tile * (int64_t)(64 * V), p.P, K, m, lane, lds_stats);
+      __syncthreads();
+    }
+    // store first, then reduce the diagnostics while the stores drain
+    if (in) {
+      float out[V];
+#pragma unroll
+      for (int t = 0; t < V; ++t) out[t] = outer ? lds_stats[t * 64 + lane] : mean[t];
+      store_v<T, V, true>(row, e, out);
+#pragma unroll
+      for (int t = 0; t < V; ++t) {
+        const double cbar = outer ? (double)xo[t] - (double)mean[t] : (double)mean[t];
+        const double c = outer ? (double)xo[t] - (double)a[t] : (double)a[t];
+        a_sq += c * c;
+        a_dot += c * cbar;
         a_var += (c - cbar) * (c - cbar);
-        a_sq[m] += c * c;
-        a_dot[m] += c * cbar;
+        if (m == 0) {
+          a_mean += cbar * cbar;
+          if (outer) a_ref += (double)xo[t] * (double)xo[t];
+        }
       }
     }
-    if (outer) outer_step<V>(p.outer, e, mean);
-    for (int32_t m = 0; m < K; ++m) store_v<T, V, true>(s + (int64_t)m * p.P, e, mean);
+    __syncthreads();
   }
-  // block reduction of every diagnostic, fixed order
-  __shared__ double red[kBlock / 64][kStatsStride];
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  double vals[kStatsStride];
-  vals[0] = a_mean;
-  vals[1] = a_var;
-  vals[2] = a_ref;
-  vals[3] = 0.0;
-#pragma unroll
-  for (int m = 0; m < kStatsMaxK; ++m) {
-    vals[4 + m] = a_sq[m];
-    vals[4 + kStatsMaxK + m] = a_dot[m];
-  }
-#pragma unroll
-  for (int k = 0; k < kStatsStride; ++k) {
-    const double w = wave_sum(vals[k]);
-    if (lane == 0) red[wave][k] = w;
+  // one partial row per workgroup, fixed order
+  const double sq = wave_sum(a_sq), dot = wave_sum(a_dot), var = wave_sum(a_var);
+  const double mn = wave_sum(a_mean), ref = wave_sum(a_ref);
+  if (lane == 0) {
+    red[m][0] = sq;
+    red[m][1] = dot;
+    red[m][2] = var;
+    red[m][3] = mn;
+    red[m][4] = ref;
   }
   __syncthreads();
   if (threadIdx.x < kStatsStride) {
-    double t = 0.0;
-#pragma unroll
-    for (int i = 0; i < kBlock / 64; ++i) t += red[i][threadIdx.x];
-    partials[((int64_t)blockIdx.y * gridDim.x + blockIdx.x) * kStatsStride + threadIdx.x] = t;
+    const int k = threadIdx.x;
+    double v = 0.0;
+    if (k == 0) v = red[0][3];
+    else if (k == 1) for (int32_t q = 0; q < K; ++q) v += red[q][2];
+    else if (k == 2) v = red[0][4];
+    else if (k >= 4 && k < 4 + kStatsMaxK) v = (k - 4 < K) ? red[k - 4][0] : 0.0;
+    else if (k >= 4 + kStatsMaxK) v = (k - 4 - kStatsMaxK < K) ? red[k - 4 - kStatsMaxK][1] : 0.0;
+    partials[((int64_t)blockIdx.y * kStatsStride + k) * gridDim.x + blockIdx.x] = v;
   }
 }
 
-// out[state][k] = sum over blocks of partials (fixed order); the variance
-// sum is divided by K.
-__global__ __launch_bounds__(64) void k_stats_finalize(const double* __restrict__ partials, int32_t nb, int32_t K,
+// out[state][k] = the sum of the nb partials of stat k of that state, one
+// workgroup per (stat, state), in a fixed order: thread-strided with four
+// independent accumulators (four loads in flight per thread), then waves
+// in order.  The variance sum is divided by K.
+__global__ __launch_bounds__(256) void k_stats_finalize(const double* __restrict__ partials, int32_t nb, int32_t K,
                                                        double* __restrict__ out) {
-  const int32_t state = blockIdx.x;
-  for (int32_t k = threadIdx.x; k < kStatsStride; k += 64) {
-    double t = 0.0;
-    for (int32_t b = 0; b < nb; ++b) t += partials[((int64_t)state * nb + b) * kStatsStride + k];
-    out[(int64_t)state * kStatsStride + k] = (k == 1) ? t / (double)K : t;
+  __shared__ double red[4];
+  const int32_t k = blockIdx.x, state = blockIdx.y;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const double* __restrict__ q = partials + ((int64_t)state * kStatsStride + k) * nb;
+  double a0 = 0.0, a1 = 0.0, a2 = 0.0, a3 = 0.0;
+  int32_t b = threadIdx.x;
+  for (; b + 3 * 256 < nb; b += 4 * 256) {
+    a0 += q[b];
+    a1 += q[b + 256];
+    a2 += q[b + 512];
+    a3 += q[b + 768];
+  }
+  for (; b < nb; b += 256) a0 += q[b];
+  const double t = wave_sum((a0 + a1) + (a2 + a3));
+  if (lane == 0) red[wave] = t;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const double sum = (red[0] + red[1]) + (red[2] + red[3]);
+    out[(int64_t)state * kStatsStride + k] = (k == 1) ? sum / (double)K : sum;
   }
 }
 

@@ -334,13 +334,34 @@ void launch_mean(MeanParams p, int nstates, int V, hipStream_t st) {
   }
 }
 
-constexpr int kStatsBlocksMax = 1024;
+constexpr int kStatsBlocksMax = 4096;
 
-int32_t stats_blocks_for(int64_t P) {
-  int64_t nb = (P + 4 * kBlock - 1) / (4 * kBlock);
-  if (nb < 1) nb = 1;
+// Workgroups per state of the diagnostics pass: enough K-wave workgroups
+// for about 16384 waves over all states of the launch (twice what the 256
+// CUs hold at 8 waves per SIMD), a multiple of 8 so every workgroup keeps
+// its XCD's pieces as it strides, and no more than there are pieces.
+int32_t stats_blocks_for(int64_t pieces, int32_t nstates, int32_t K) {
+  int64_t nb = (16384 + (int64_t)nstates * K - 1) / ((int64_t)nstates * K);
+  nb = (nb + 7) / 8 * 8;
   if (nb > kStatsBlocksMax) nb = kStatsBlocksMax;
-  return (int32_t)nb;
+  if (nb > pieces) nb = pieces;
+  return (int32_t)(nb < 1 ? 1 : nb);
+}
+
+// The diagnostics pass of nstates states of one storage type: V elements
+// per lane (16-byte accesses, or 1 when a row length breaks alignment),
+// K waves per workgroup, then the fixed-order finalize into out.
+template <typename T>
+void launch_stats(MeanParams q, int nstates, int V, double* partials, double* out, hipStream_t st) {
+  const int64_t per = (int64_t)64 * V;
+  q.tiles = (q.P + per - 1) / per;
+  const int32_t nb = stats_blocks_for(q.tiles, nstates, q.K);
+  const dim3 grid(nb, nstates), block(64 * q.K);
+  const size_t lds = (size_t)q.K * 64 * V * sizeof(float);
+  constexpr int VV = sizeof(T) == 2 ? 8 : 4;
+  if (V == 1) hipLaunchKernelGGL((k_replica_mean_stats<T, 1>), grid, block, lds, st, q, partials);
+  else hipLaunchKernelGGL((k_replica_mean_stats<T, VV>), grid, block, lds, st, q, partials);
+  hipLaunchKernelGGL(k_stats_finalize, dim3(kStatsStride, nstates), dim3(256), 0, st, partials, nb, q.K, out);
 }
 
 size_t stats_scratch_for(const mtdao_config& c) {
@@ -685,7 +706,6 @@ int32_t mtdao_sync_stats(mtdao_handle* h, uint32_t mask, uint32_t* applied_mask,
   double* partials = reinterpret_cast<double*>(scratch);
   const size_t part_per_state = (size_t)kStatsBlocksMax * kStatsStride;
   double* out = partials + (size_t)(2 + c.n_moments + 1) * part_per_state;  // [2][nslots][stride]
-  const int32_t nb = stats_blocks_for(c.numel);
   // state ids of the fp32 launch, in launch order
   int ids[2 + kMaxN];
   MeanParams mp;
@@ -709,31 +729,15 @@ int32_t mtdao_sync_stats(mtdao_handle* h, uint32_t mask, uint32_t* applied_mask,
     ids[n] = c.n_moments + 1;
     mp.state[n++] = h->v;
   }
-  const bool fp32_vec = c.numel % 4 == 0, bf16_vec = c.numel % 4 == 0;  // 16-byte / 8-byte slots
-  if (n > 0) {
-    MeanParams q = mp;
-    q.tiles = fp32_vec ? tiles_for<4 * kBlock, piece_for(4)>(c.numel) : tiles_for<kBlock, piece_for(1)>(c.numel);
-    if (fp32_vec)
-      hipLaunchKernelGGL((k_replica_mean_stats<float, 4, piece_for(4)>), dim3(nb, n), dim3(kBlock), 0, st, q, partials);
-    else
-      hipLaunchKernelGGL((k_replica_mean_stats<float, 1, piece_for(1)>), dim3(nb, n), dim3(kBlock), 0, st, q, partials);
-    hipLaunchKernelGGL(k_stats_finalize, dim3(n), dim3(64), 0, st, partials, nb, c.replicas, out);
-  }
+  if (n > 0) launch_stats<float>(mp, n, vec_width(MTDAO_F32, c.numel), partials, out, st);
   const bool bf16_x = (m & 1u) && c.param_dtype == MTDAO_BF16;
   if (bf16_x) {
     MeanParams q = mp;
     std::memset(q.state, 0, sizeof q.state);
     q.state[0] = h->x;
     q.outer_state = h->x_outer ? 0 : -1;
-    q.tiles = bf16_vec ? tiles_for<4 * kBlock, piece_for(4)>(c.numel) : tiles_for<kBlock, piece_for(1)>(c.numel);
     double* part_x = partials + (size_t)(2 + c.n_moments) * part_per_state;
-    if (bf16_vec)
-      hipLaunchKernelGGL((k_replica_mean_stats<uint16_t, 4, piece_for(4)>), dim3(nb, 1), dim3(kBlock), 0, st, q,
-                         part_x);
-    else
-      hipLaunchKernelGGL((k_replica_mean_stats<uint16_t, 1, piece_for(1)>), dim3(nb, 1), dim3(kBlock), 0, st, q,
-                         part_x);
-    hipLaunchKernelGGL(k_stats_finalize, dim3(1), dim3(64), 0, st, part_x, nb, c.replicas, out + nslots * kStatsStride);
+    launch_stats<uint16_t>(q, 1, vec_width(MTDAO_BF16, c.numel), part_x, out + nslots * kStatsStride, st);
   }
   r = hip_check(&h->err, hipGetLastError(), "mtdao_sync_stats launch");
   if (r != MTDAO_OK) return r;
