@@ -904,13 +904,21 @@ constexpr int kStatsStride = 4 + 2 * kStatsMaxK;  // doubles per state (layout i
 // sum_m ||c^m - cbar||^2, ||xo||^2, ||c^m||^2 and <c^m, cbar>, with
 // c^m = S^m, or c^m = xo - x^m for x under a Nesterov OuterOpt.
 // blockDim = 64 K (1 <= K <= kStatsMaxK), dynamic LDS of K * 64 * V
-// floats; a fixed grid of workgroups walks the pieces, each wave keeping
-// fp64 sums for its own replica (wave 0 also those of cbar and xo), and
-// every workgroup writes one partial of each of the kStatsStride sums
-// (partials[state][stat][workgroup]), reduced in a fixed order:
-// deterministic for a given grid.
+// floats.  Workgroup b takes q pieces of 64 V elements, pieces
+// ((b / 8) q + i) 8 + b mod 8 for i < q: each XCD keeps one piece in eight,
+// and as workgroups are dispatched in order the pieces in flight stay a
+// compact window, as in the plain mean (a fixed grid of workgroups
+// striding over the row scattered them and ran 30% slower).  Each wave
+// keeps fp64 sums for its own replica (wave 0 also those of cbar and xo)
+// and the workgroup writes its kStatsSums(K) sums, contiguous, to
+// partials[state][workgroup][sum]:
+//   0 ||cbar||^2, 1 sum_m ||c^m - cbar||^2, 2 ||xo||^2,
+//   3 + m ||c^m||^2, 3 + K + m <c^m, cbar>.
+__host__ __device__ constexpr int kStatsSums(int K) { return 3 + 2 * K; }
+
 template <typename T, int V>
-__global__ __launch_bounds__(64 * kStatsMaxK) void k_replica_mean_stats(MeanParams p, double* __restrict__ partials) {
+__global__ __launch_bounds__(64 * kStatsMaxK) void k_replica_mean_stats(MeanParams p, int32_t q,
+                                                                          double* __restrict__ partials) {
   extern __shared__ float lds_stats[];  // [K][64 V]
   __shared__ double red[kStatsMaxK][5];
   T* __restrict__ s = reinterpret_cast<T*>(p.state[blockIdx.y]);
@@ -919,30 +927,17 @@ __global__ __launch_bounds__(64 * kStatsMaxK) void k_replica_mean_stats(MeanPara
   const double rk = 1.0 / (double)K;
   T* __restrict__ row = s + (int64_t)m * p.P;
   double a_sq = 0.0, a_dot = 0.0, a_var = 0.0, a_mean = 0.0, a_ref = 0.0;
-  // the loads of the next piece are issued before the current one is
-  // averaged and reduced, so each wave keeps a piece in flight through the
-  // barriers of the current one
-  float na[V], nxo[V];
-  {
-    const int64_t e = (int64_t)blockIdx.x * (64 * V) + (int64_t)lane * V;
-    if (blockIdx.x < p.tiles && e < p.P) {
-      load_v<T, V, true>(row, e, na);
-      if (outer) load_v<float, V, false>(p.outer.xo, e, nxo);
-    }
-  }
-  for (int64_t tile = blockIdx.x; tile < p.tiles; tile += gridDim.x) {
+  for (int32_t i = 0; i < q; ++i) {
+    const int64_t tile = ((int64_t)(blockIdx.x >> 3) * q + i) * 8 + (blockIdx.x & 7);
+    if (tile >= p.tiles) break;  // uniform over the workgroup
     const int64_t e = tile * (int64_t)(64 * V) + (int64_t)lane * V;
     const bool in = e < p.P;
     float a[V], xo[V];
 #pragma unroll
-    for (int t = 0; t < V; ++t) {
-      a[t] = in ? na[t] : 0.0f;
-      xo[t] = (in && outer) ? nxo[t] : 0.0f;
-    }
-    const int64_t en = e + (int64_t)gridDim.x * (64 * V);
-    if (tile + gridDim.x < p.tiles && en < p.P) {
-      load_v<T, V, true>(row, en, na);
-      if (outer) load_v<float, V, false>(p.outer.xo, en, nxo);
+    for (int t = 0; t < V; ++t) a[t] = xo[t] = 0.0f;
+    if (in) {
+      load_v<T, V, true>(row, e, a);
+      if (outer) load_v<float, V, false>(p.outer.xo, e, xo);
     }
 #pragma unroll
     for (int t = 0; t < V; ++t) lds_stats[(m * V + t) * 64 + lane] = a[t];
@@ -983,7 +978,7 @@ __global__ __launch_bounds__(64 * kStatsMaxK) void k_replica_mean_stats(MeanPara
     }
     __syncthreads();
   }
-  // one partial row per workgroup, fixed order
+  // the workgroup's sums, fixed order
   const double sq = wave_sum(a_sq), dot = wave_sum(a_dot), var = wave_sum(a_var);
   const double mn = wave_sum(a_mean), ref = wave_sum(a_ref);
   if (lane == 0) {
@@ -994,43 +989,86 @@ __global__ __launch_bounds__(64 * kStatsMaxK) void k_replica_mean_stats(MeanPara
     red[m][4] = ref;
   }
   __syncthreads();
-  if (threadIdx.x < kStatsStride) {
+  const int ns = kStatsSums(K);
+  if ((int)threadIdx.x < ns) {
     const int k = threadIdx.x;
     double v = 0.0;
     if (k == 0) v = red[0][3];
     else if (k == 1) for (int32_t q = 0; q < K; ++q) v += red[q][2];
     else if (k == 2) v = red[0][4];
-    else if (k >= 4 && k < 4 + kStatsMaxK) v = (k - 4 < K) ? red[k - 4][0] : 0.0;
-    else if (k >= 4 + kStatsMaxK) v = (k - 4 - kStatsMaxK < K) ? red[k - 4 - kStatsMaxK][1] : 0.0;
-    partials[((int64_t)blockIdx.y * kStatsStride + k) * gridDim.x + blockIdx.x] = v;
+    else if (k < 3 + K) v = red[k - 3][0];
+    else v = red[k - 3 - K][1];
+    partials[((int64_t)blockIdx.y * gridDim.x + blockIdx.x) * ns + k] = v;
   }
 }
 
-// out[state][k] = the sum of the nb partials of stat k of that state, one
-// workgroup per (stat, state), in a fixed order: thread-strided with four
-// independent accumulators (four loads in flight per thread), then waves
-// in order.  The variance sum is divided by K.
-__global__ __launch_bounds__(256) void k_stats_finalize(const double* __restrict__ partials, int32_t nb, int32_t K,
-                                                       double* __restrict__ out) {
-  __shared__ double red[4];
-  const int32_t k = blockIdx.x, state = blockIdx.y;
+// Fixed-order reduction of the workgroup sums, in two levels.  Each thread
+// adds whole rows of kStatsSums(K) sums (contiguous in memory) in row
+// order, keeping every sum in its own fp64 register, then the block adds
+// the threads' totals wave by wave in order.
+constexpr int kStatsChunk = 8192;
+constexpr int kStatsMaxSums = 3 + 2 * kStatsMaxK;
+
+__device__ __forceinline__ void stats_block_sum(double (&acc)[kStatsMaxSums], int ns, double* __restrict__ dst) {
+  __shared__ double red[4][kStatsMaxSums];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const double* __restrict__ q = partials + ((int64_t)state * kStatsStride + k) * nb;
-  double a0 = 0.0, a1 = 0.0, a2 = 0.0, a3 = 0.0;
-  int32_t b = threadIdx.x;
-  for (; b + 3 * 256 < nb; b += 4 * 256) {
-    a0 += q[b];
-    a1 += q[b + 256];
-    a2 += q[b + 512];
-    a3 += q[b + 768];
+#pragma unroll
+  for (int k = 0; k < kStatsMaxSums; ++k) {
+    if (k < ns) {
+      const double w = wave_sum(acc[k]);
+      if (lane == 0) red[wave][k] = w;
+    }
   }
-  for (; b < nb; b += 256) a0 += q[b];
-  const double t = wave_sum((a0 + a1) + (a2 + a3));
-  if (lane == 0) red[wave] = t;
   __syncthreads();
-  if (threadIdx.x == 0) {
-    const double sum = (red[0] + red[1]) + (red[2] + red[3]);
-    out[(int64_t)state * kStatsStride + k] = (k == 1) ? sum / (double)K : sum;
+  if ((int)threadIdx.x < ns) {
+    const int k = threadIdx.x;
+    dst[k] = (red[0][k] + red[1][k]) + (red[2][k] + red[3][k]);
+  }
+}
+
+// Level 1: chunk blockIdx.x (kStatsChunk consecutive workgroup rows) of
+// state blockIdx.y into level1[state][chunk][sum].
+__global__ __launch_bounds__(256) void k_stats_reduce(const double* __restrict__ partials, int64_t nb, int32_t ns,
+                                                     double* __restrict__ level1) {
+  double acc[kStatsMaxSums];
+#pragma unroll
+  for (int k = 0; k < kStatsMaxSums; ++k) acc[k] = 0.0;
+  const double* __restrict__ q = partials + (int64_t)blockIdx.y * nb * ns;
+  const int64_t lo = (int64_t)blockIdx.x * kStatsChunk;
+  const int64_t hi = lo + kStatsChunk < nb ? lo + kStatsChunk : nb;
+  for (int64_t b = lo + threadIdx.x; b < hi; b += 256) {
+#pragma unroll
+    for (int k = 0; k < kStatsMaxSums; ++k)
+      if (k < ns) acc[k] += q[b * ns + k];
+  }
+  stats_block_sum(acc, ns, level1 + ((int64_t)blockIdx.y * gridDim.x + blockIdx.x) * ns);
+}
+
+// Level 2: the nc chunk rows of state blockIdx.x, in chunk order, into out
+// in the layout of mtdao.h (kStatsStride doubles per state; slot 3 and the
+// slots of workers m >= K are 0); the variance sum is divided by K.
+__global__ __launch_bounds__(256) void k_stats_finalize(const double* __restrict__ level1, int32_t nc, int32_t K,
+                                                       double* __restrict__ out) {
+  __shared__ double tot[kStatsMaxSums];
+  const int32_t state = blockIdx.x, ns = kStatsSums(K);
+  double acc[kStatsMaxSums];
+#pragma unroll
+  for (int k = 0; k < kStatsMaxSums; ++k) acc[k] = 0.0;
+  const double* __restrict__ q = level1 + (int64_t)state * nc * ns;
+  for (int32_t c = threadIdx.x; c < nc; c += 256) {
+#pragma unroll
+    for (int k = 0; k < kStatsMaxSums; ++k)
+      if (k < ns) acc[k] += q[(int64_t)c * ns + k];
+  }
+  stats_block_sum(acc, ns, tot);
+  __syncthreads();
+  if (threadIdx.x < kStatsStride) {
+    const int k = threadIdx.x;
+    double t = 0.0;
+    if (k < 3) t = tot[k];
+    else if (k >= 4 && k < 4 + K) t = tot[3 + (k - 4)];
+    else if (k >= 4 + kStatsMaxK && k < 4 + kStatsMaxK + K) t = tot[3 + K + (k - 4 - kStatsMaxK)];
+    out[(int64_t)state * kStatsStride + k] = (k == 1) ? t / (double)K : t;
   }
 }
 

@@ -4,6 +4,7 @@
 
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -334,41 +335,50 @@ void launch_mean(MeanParams p, int nstates, int V, hipStream_t st) {
   }
 }
 
-constexpr int kStatsBlocksMax = 4096;
-
-// Workgroups per state of the diagnostics pass: enough K-wave workgroups
-// for about 16384 waves over all states of the launch (twice what the 256
-// CUs hold at 8 waves per SIMD), a multiple of 8 so every workgroup keeps
-// its XCD's pieces as it strides, and no more than there are pieces.
-int32_t stats_blocks_for(int64_t pieces, int32_t nstates, int32_t K) {
-  int64_t nb = (16384 + (int64_t)nstates * K - 1) / ((int64_t)nstates * K);
-  nb = (nb + 7) / 8 * 8;
-  if (nb > kStatsBlocksMax) nb = kStatsBlocksMax;
-  if (nb > pieces) nb = pieces;
-  return (int32_t)(nb < 1 ? 1 : nb);
-}
-
 // The diagnostics pass of nstates states of one storage type: V elements
-// per lane (16-byte accesses, or 1 when a row length breaks alignment),
-// K waves per workgroup, then the fixed-order finalize into out.
+// per lane (16-byte accesses, or 1 when a row length breaks alignment), K
+// waves per workgroup, kStatsPieces pieces per workgroup, then the two
+// fixed-order reduction levels into out.  partials holds
+// nstates * kStatsSums(K) * (workgroups + chunks) doubles.
+//
+// Pieces per workgroup, measured on MI355X at 1.31B params x 4 replicas
+// (one state): 1 -> 14.5 ms (the workgroup's closing reduction dominates),
+// 4 -> 7.5 ms, 16 -> 7.7 ms, 64 -> 8.0 ms, 1024 -> 8.4 ms.
+constexpr int32_t kStatsPieces = 4;
+int64_t stats_pieces(int64_t P, int V) { return (P + 64 * V - 1) / (64 * V); }
+int64_t stats_blocks(int64_t pieces) { return (pieces + 8 * kStatsPieces - 1) / (8 * kStatsPieces) * 8; }
+int64_t stats_chunks(int64_t nb) { return (nb + kStatsChunk - 1) / kStatsChunk; }
+
 template <typename T>
 void launch_stats(MeanParams q, int nstates, int V, double* partials, double* out, hipStream_t st) {
-  const int64_t per = (int64_t)64 * V;
-  q.tiles = (q.P + per - 1) / per;
-  const int32_t nb = stats_blocks_for(q.tiles, nstates, q.K);
-  const dim3 grid(nb, nstates), block(64 * q.K);
+  q.tiles = stats_pieces(q.P, V);
+  const dim3 grid((unsigned)stats_blocks(q.tiles), nstates), block(64 * q.K);
+  const int64_t nb = grid.x, nc = stats_chunks(nb);
+  const int32_t ns = kStatsSums(q.K);
+  double* level1 = partials + (size_t)nstates * ns * nb;
   const size_t lds = (size_t)q.K * 64 * V * sizeof(float);
   constexpr int VV = sizeof(T) == 2 ? 8 : 4;
-  if (V == 1) hipLaunchKernelGGL((k_replica_mean_stats<T, 1>), grid, block, lds, st, q, partials);
-  else hipLaunchKernelGGL((k_replica_mean_stats<T, VV>), grid, block, lds, st, q, partials);
-  hipLaunchKernelGGL(k_stats_finalize, dim3(kStatsStride, nstates), dim3(256), 0, st, partials, nb, q.K, out);
+  if (V == 1) hipLaunchKernelGGL((k_replica_mean_stats<T, 1>), grid, block, lds, st, q, kStatsPieces, partials);
+  else hipLaunchKernelGGL((k_replica_mean_stats<T, VV>), grid, block, lds, st, q, kStatsPieces, partials);
+  hipLaunchKernelGGL(k_stats_reduce, dim3((unsigned)nc, nstates), dim3(256), 0, st, partials, nb, ns, level1);
+  hipLaunchKernelGGL(k_stats_finalize, dim3(nstates), dim3(256), 0, st, level1, (int32_t)nc, q.K, out);
+}
+
+// Doubles of the diagnostics scratch for up to 2 + N fp32 states and a bf16
+// x: each launch's partials and chunk sums, then the finalized rows of the
+// two launches.
+size_t stats_scratch_doubles(const mtdao_config& c, size_t* fp32_part, size_t* bf16_part) {
+  const int64_t ns = kStatsSums(c.replicas);
+  const int64_t nb32 = stats_blocks(stats_pieces(c.numel, vec_width(MTDAO_F32, c.numel)));
+  const int64_t nb16 = stats_blocks(stats_pieces(c.numel, vec_width(MTDAO_BF16, c.numel)));
+  *fp32_part = (size_t)(2 + c.n_moments) * ns * (nb32 + stats_chunks(nb32));
+  *bf16_part = c.param_dtype == MTDAO_BF16 ? (size_t)ns * (nb16 + stats_chunks(nb16)) : 0;
+  return *fp32_part + *bf16_part + (size_t)2 * (2 + kMaxN) * kStatsStride;
 }
 
 size_t stats_scratch_for(const mtdao_config& c) {
-  // partials of up to 2 + N states (fp32 launch) + 1 (bf16 x launch), then the
-  // finalized rows of both launches
-  const size_t states = (size_t)(2 + c.n_moments + 1);
-  return states * kStatsBlocksMax * kStatsStride * sizeof(double) + 2 * (2 + kMaxN) * kStatsStride * sizeof(double);
+  size_t a, b;
+  return stats_scratch_doubles(c, &a, &b) * sizeof(double);
 }
 
 int launch_blocks(int64_t n) {
@@ -704,8 +714,10 @@ int32_t mtdao_sync_stats(mtdao_handle* h, uint32_t mask, uint32_t* applied_mask,
   if (m == 0 || c.numel == 0) return MTDAO_OK;
   hipStream_t st = reinterpret_cast<hipStream_t>(hip_stream);
   double* partials = reinterpret_cast<double*>(scratch);
-  const size_t part_per_state = (size_t)kStatsBlocksMax * kStatsStride;
-  double* out = partials + (size_t)(2 + c.n_moments + 1) * part_per_state;  // [2][nslots][stride]
+  size_t fp32_part, bf16_part;
+  stats_scratch_doubles(c, &fp32_part, &bf16_part);
+  double* part_x = partials + fp32_part;
+  double* out = part_x + bf16_part;  // [2][nslots][stride]
   // state ids of the fp32 launch, in launch order
   int ids[2 + kMaxN];
   MeanParams mp;
@@ -736,7 +748,6 @@ int32_t mtdao_sync_stats(mtdao_handle* h, uint32_t mask, uint32_t* applied_mask,
     std::memset(q.state, 0, sizeof q.state);
     q.state[0] = h->x;
     q.outer_state = h->x_outer ? 0 : -1;
-    double* part_x = partials + (size_t)(2 + c.n_moments) * part_per_state;
     launch_stats<uint16_t>(q, 1, vec_width(MTDAO_BF16, c.numel), part_x, out + nslots * kStatsStride, st);
   }
   r = hip_check(&h->err, hipGetLastError(), "mtdao_sync_stats launch");
