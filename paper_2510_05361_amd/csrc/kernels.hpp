@@ -671,6 +671,87 @@ __global__ __launch_bounds__(kBlock) void k_sgdm_averaged_momenta(StepParams p, 
   }
 }
 
+// The same step with one wavefront per replica (blockDim = 64 K,
+// 1 < K <= kWaveMaxK), in one pass: wave m loads g, x and every u^j of
+// replica m once, updates its moments, and each due moment meets its
+// replicas' values in LDS, where column t is averaged by wave t mod K (the
+// mean_add / mean_of order of every averaging kernel) and read back by
+// every wave before the direction uses it; x is updated and, when due,
+// averaged the same way.  The values equal k_sgdm_averaged_momenta's bit
+// for bit; that kernel re-reads g (and the moments not due) in its second
+// pass.  Barriers are reached by every thread, also in the row tail.
+template <int N, typename XT, typename GT, int V, int NTM>
+__global__ __launch_bounds__(64 * kWaveMaxK) __attribute__((amdgpu_waves_per_eu(8)))
+void k_sgdm_averaged_momenta_waves(StepParams p, uint32_t mask, int32_t K) {
+#pragma clang fp contract(off)
+  constexpr bool NTL = (NTM & 1) != 0, NTS = (NTM & 2) != 0;
+  __shared__ float lds[kWaveMaxK][64 * V];
+  const int32_t m = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  XT* __restrict__ x = reinterpret_cast<XT*>(p.x);
+  const GT* __restrict__ g = reinterpret_cast<const GT*>(p.g);
+  const double rk = 1.0 / (double)K;
+  const float sc = p.scale != nullptr ? p.scale[m] : 1.0f;
+
+  // the mean over the replicas of val (this wave's row values), through
+  // LDS, written back into val
+  auto average = [&](float (&val)[V], bool in) {
+#pragma unroll
+    for (int t = 0; t < V; ++t) lds[m][t * 64 + lane] = val[t];
+    __syncthreads();
+    for (int t = m; in && t < V; t += K) {
+      const float s0 = lds[0][t * 64 + lane];
+      double d = 0.0;
+#pragma unroll 4
+      for (int32_t q = 1; q < K; ++q) mean_add(d, lds[q][t * 64 + lane], s0);
+      lds[0][t * 64 + lane] = mean_of(s0, d, rk);
+    }
+    __syncthreads();
+#pragma unroll
+    for (int t = 0; t < V; ++t) val[t] = lds[0][t * 64 + lane];
+    __syncthreads();
+  };
+
+  for (int64_t tile = blockIdx.x; tile < p.tiles; tile += gridDim.x) {
+    const int64_t e = tile * (int64_t)(64 * V) + (int64_t)lane * V;
+    const bool in = e < p.P;
+    const int64_t r = (int64_t)m * p.P + e;
+    float gv[V], xv[V], uv[N][V];
+#pragma unroll
+    for (int t = 0; t < V; ++t) gv[t] = xv[t] = 0.0f;
+#pragma unroll
+    for (int j = 0; j < N; ++j)
+#pragma unroll
+      for (int t = 0; t < V; ++t) uv[j][t] = 0.0f;
+    if (in) {
+      load_v<GT, V, NTL>(g, r, gv);
+      load_v<XT, V, NTL>(x, r, xv);
+#pragma unroll
+      for (int j = 0; j < N; ++j) load_v<float, V, NTL>(p.u[j], r, uv[j]);
+    }
+#pragma unroll
+    for (int t = 0; t < V; ++t) {
+      const float gh = sc * gv[t];
+#pragma unroll
+      for (int j = 0; j < N; ++j) uv[j][t] = __builtin_fmaf(p.beta[j], uv[j][t], p.omb[j] * gh);
+    }
+#pragma unroll
+    for (int j = 0; j < N; ++j) {
+      if ((mask >> (j + 1)) & 1u) average(uv[j], in);
+      if (in) store_v<float, V, NTS>(p.u[j], r, uv[j]);
+    }
+#pragma unroll
+    for (int t = 0; t < V; ++t) {
+      const float gh = sc * gv[t];
+      float delta = p.gw * gh;
+#pragma unroll
+      for (int j = 0; j < N; ++j) delta = __builtin_fmaf(p.w[j], uv[j][t], delta);
+      xv[t] = as_stored<XT>(__builtin_fmaf(-p.lr, delta, xv[t]));
+    }
+    if (mask & 1u) average(xv, in);
+    if (in) store_v<XT, V, NTS>(x, r, xv);
+  }
+}
+
 // ADOPT's first update with the previous-v order: v = g^2, nothing else.
 template <typename GT, int V, int U, bool NT>
 __global__ __launch_bounds__(kBlock) void k_adopt_init_v(const void* gp, float* vp, int64_t P, int64_t tiles) {

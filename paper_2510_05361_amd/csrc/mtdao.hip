@@ -395,6 +395,14 @@ void launch_sgdm_averaged_momenta(const mtdao_config& c, StepParams p, int V, ui
     if constexpr (FORM == kSgdm) {
       using XT = typename decltype(xt)::type;
       using GT = typename decltype(gt)::type;
+      if (c.replicas > 1 && c.replicas <= kWaveMaxK) {
+        // one wavefront per replica, one pass
+        const int64_t per = (int64_t)64 * VV;
+        p.tiles = (p.P + per - 1) / per;
+        hipLaunchKernelGGL((k_sgdm_averaged_momenta_waves<N, XT, GT, VV, kStepNT>), grid_for(p.tiles, 1),
+                           dim3(64 * c.replicas), 0, st, p, mask, c.replicas);
+        return;
+      }
       constexpr int C = piece_for(VV);
       p.tiles = tiles_for<kBlock * VV, C>(p.P);
       hipLaunchKernelGGL((k_sgdm_averaged_momenta<N, XT, GT, VV, kStepNT, C>), grid_for(p.tiles, 1), dim3(kBlock), 0,

@@ -405,12 +405,13 @@ def _prob_workload(name, **kw):
     return w if name == "full" else synth.small_variant(w, 60_000, tail=37 if name == "odd" else 40)
 
 
-@pytest.mark.parametrize("size", ["aligned", "odd", "full"])
+@pytest.mark.parametrize("size", ["aligned", "odd", "full", "k17"])
 def test_probabilistic_sync_against_oracle(size):
     """Bernoulli averaging events (p_x = 1/16, p_u = 1/4, 1/32; drawn on the
     host) through mtdao_step_sync with the averaged-momenta order, against
-    the oracle's Algorithm 4 on the same events."""
-    w = _prob_workload(size, steps=40 if size == "full" else 64)
+    the oracle's Algorithm 4 on the same events.  K = 16 runs the
+    wave-per-replica kernel, K = 17 the thread-per-column one."""
+    w = _prob_workload(size, steps=40 if size == "full" else 64, **({"replicas": 17} if size == "k17" else {}))
     masks = synth.bernoulli_masks(123, w.steps, 2, 1 / 16, (1 / 4, 1 / 32))
     assert any(m & 0b010 for m in masks) and any(m & 1 for m in masks)
     log(f"case prob {size} P={w.numel} K={w.replicas} masks={sum(1 for m in masks if m)}")
