@@ -61,11 +61,18 @@ def norm_bytes_per_element(w) -> int:
 
 
 def kernel_hash() -> str:
-    """Hash of the kernel source and its launch configuration."""
+    """Hash of the kernel source and its launch configuration (kernels.hpp
+    and mtdao.hip with comments removed and white space collapsed, so that
+    a change of wording leaves it alone and a change of code does not)."""
+    import re
+
     h = hashlib.sha256()
     for p in KERNEL_SRCS:
-        with open(p, "rb") as f:
-            h.update(f.read())
+        with open(p, encoding="utf-8") as f:
+            text = f.read()
+        text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+        text = re.sub(r"//[^\n]*", " ", text)
+        h.update(" ".join(text.split()).encode())
     return h.hexdigest()[:16]
 
 

@@ -6,9 +6,14 @@
 // one replica row per vector slot, so loads and stores are 16-byte vector
 // accesses and a 64-lane wavefront moves 1 KiB per instruction; all loads
 // of a tile are issued before any of them is consumed.  Rows are
-// replica-major [K][P]; blockIdx.y is the replica (or the state, for the
-// mean), blockIdx.x strides over tiles of 256*V*U elements of the row,
-// placed on the row by tile_elem().
+// replica-major [K][P].  Two organisations:
+//   - one replica row per workgroup (the plain step, the norm pass, the
+//     thread-per-column kernels): blockIdx.y is the replica (the state,
+//     for the mean), blockIdx.x a tile of the row placed by tile_elem();
+//   - one wavefront per replica (the fused step + sync, the mean, the
+//     diagnostics and Algorithm 4's step for 1 < K <= 16): a workgroup of
+//     K waves takes one piece of 64 V elements of every row, and values
+//     that must be averaged meet in LDS.
 #pragma once
 
 #include <hip/hip_runtime.h>

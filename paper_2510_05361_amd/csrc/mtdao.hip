@@ -309,29 +309,26 @@ void launch_norm(const void* g, int64_t P, int32_t K, int V, int32_t nb, double*
 
 template <typename T>
 void launch_mean(MeanParams p, int nstates, int V, hipStream_t st) {
+  constexpr int VW = sizeof(T) == 2 ? 8 : 4;  // elements of a 16-byte slot
   if (p.K > 1 && p.K <= kWaveMaxK) {
     // one wavefront per replica, one piece of 64 V elements per workgroup
-    const int VW = V == 1 ? 1 : (sizeof(T) == 2 ? 8 : 4);
-    p.tiles = (p.P + 64 * VW - 1) / (64 * VW);
+    const int vw = V == 1 ? 1 : VW;
+    p.tiles = (p.P + 64 * vw - 1) / (64 * vw);
     const dim3 grid = grid_for(p.tiles, nstates), block(64 * p.K);
-    const size_t lds = (size_t)p.K * 64 * VW * sizeof(float);
-    constexpr int VV = sizeof(T) == 2 ? 8 : 4;
-    if (VW == 1) hipLaunchKernelGGL((k_replica_mean_waves<T, 1, kMeanNT>), grid, block, lds, st, p);
-    else hipLaunchKernelGGL((k_replica_mean_waves<T, VV, kMeanNT>), grid, block, lds, st, p);
+    const size_t lds = (size_t)p.K * 64 * vw * sizeof(float);
+    if (vw == 1) hipLaunchKernelGGL((k_replica_mean_waves<T, 1, kMeanNT>), grid, block, lds, st, p);
+    else hipLaunchKernelGGL((k_replica_mean_waves<T, VW, kMeanNT>), grid, block, lds, st, p);
     return;
   }
+  // K = 1 (an outer step only) and K > kWaveMaxK: one thread per column
   if (V == 1) {
     p.tiles = tiles_for<kBlock, piece_for(1)>(p.P);
     hipLaunchKernelGGL((k_replica_mean<T, 1, kMeanNT, 1, piece_for(1)>), grid_for(p.tiles, nstates), dim3(kBlock), 0,
                        st, p);
-  } else if (V == 4) {
-    p.tiles = tiles_for<4 * kBlock, piece_for(4)>(p.P);
-    hipLaunchKernelGGL((k_replica_mean<T, 4, kMeanNT, 1, piece_for(4)>), grid_for(p.tiles, nstates), dim3(kBlock), 0,
-                       st, p);
   } else {
-    p.tiles = tiles_for<8 * kBlock, piece_for(8)>(p.P);
-    hipLaunchKernelGGL((k_replica_mean<T, 8, kMeanNT, 1, piece_for(8)>), grid_for(p.tiles, nstates), dim3(kBlock), 0,
-                       st, p);
+    p.tiles = tiles_for<VW * kBlock, piece_for(VW)>(p.P);
+    hipLaunchKernelGGL((k_replica_mean<T, VW, kMeanNT, 1, piece_for(VW)>), grid_for(p.tiles, nstates), dim3(kBlock),
+                       0, st, p);
   }
 }
 
