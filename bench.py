@@ -353,9 +353,9 @@ def measure_row(args) -> int:
         prob_all_s = _time_calls(lambda: opt.step_sync(grads, w.lr, 0.0, mom | 1), reps, st)
         ceil = achievable()
         parts.append(_part("step with every momentum averaged in the step", prob_u_s, step_bytes,
-                           "k_sgdm_averaged_momenta", ceil["copy_GBps"]))
+                           "k_sgdm_averaged_momenta_waves (K <= 16)", ceil["copy_GBps"]))
         parts.append(_part("step with momenta and x averaged", prob_all_s, step_bytes,
-                           "k_sgdm_averaged_momenta", ceil["copy_GBps"]))
+                           "k_sgdm_averaged_momenta_waves (K <= 16)", ceil["copy_GBps"]))
     opt.close()
     out = {"row": args.row, "workload": w.name, "replicas": K, "params_per_replica": P, "form": w.form,
            "reps": reps, "plain_step": _part("plain local step, same buffers", plain_s, step_bytes, "k_local_step",

@@ -177,8 +177,10 @@ typedef struct mtdao_buffers {
 typedef struct mtdao_handle mtdao_handle;
 
 /* Device workspace (bytes) that mtdao_init needs for this configuration:
- * per-replica clip factors and the partial sums of the gradient-norm
- * reduction (clip_rho > 0), 0 otherwise.  Host-only; no GPU needed. */
+ * with clip_rho > 0 (Adam, SGDM) the K clip factors (padded to 256 bytes)
+ * and one fp64 partial sum of the gradient-norm reduction per 8192
+ * elements of every row, about K * P / 1024 bytes; 0 otherwise.
+ * Host-only; no GPU needed. */
 int32_t mtdao_workspace_bytes(const mtdao_config* cfg, size_t* bytes);
 
 /* Validate cfg and build a handle over the caller's buffers.  With
@@ -226,7 +228,10 @@ int32_t mtdao_step_sync(mtdao_handle* h, const void* grads, float lr, float adop
                         uint32_t* applied_mask, void* hip_stream);
 
 /* Device scratch (bytes) that mtdao_sync_stats needs for this
- * configuration (per-block partial sums of the diagnostics).  Host-only. */
+ * configuration: the 3 + 2K fp64 sums of every workgroup of the
+ * diagnostics pass (one workgroup per 1024 fp32 or 2048 bf16 elements of a
+ * row) for up to N + 2 states, about (N + 2) (3 + 2K) P / 128 bytes, plus
+ * their chunk sums and the finalized rows.  Host-only. */
 int32_t mtdao_stats_scratch_bytes(const mtdao_config* cfg, size_t* bytes);
 
 /* mtdao_sync(mask) that also returns the averaging diagnostics of every
