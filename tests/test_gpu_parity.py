@@ -588,6 +588,50 @@ def test_sync_stats_against_oracle(name, outer):
     b.close()
 
 
+@pytest.mark.parametrize("outer", [None, (0.7, 0.9)], ids=["plain", "nesterov"])
+def test_sync_stats_full_size_multi_chunk(outer):
+    """mtdao_sync_stats on the full 16.8M-parameter K=4 workload, where the
+    workgroup sums span several chunks of both reduction levels: every
+    state's diagnostics against the oracle on all elements, and the averaged
+    states bit-identical to mtdao_sync."""
+    w = synth.WORKLOADS["adam_n3_k4_p16m"].replace(steps=4, period_x=2, period_u=(2, 4, 4), period_v=4)
+    log(f"case stats full P={w.numel} K={w.replicas} outer={outer}")
+    d = torch.device("cuda:0")
+    dev = DeviceInputs(w, d)
+    from gpu_harness import gpu_config, oracle_cfg
+    a = MtdaoOptimizer(gpu_config(w, 0, outer), d, x0=dev.x0_row())
+    b = MtdaoOptimizer(gpu_config(w, 0, outer), d, x0=dev.x0_row())
+    ocfg = oracle_cfg(w, outer)
+    ost = oracle.new_state(ocfg, synth.host_x0_row(w), w.replicas)
+    grads = torch.empty((w.replicas, w.numel), dtype=torch.float32, device=d)
+    K = w.replicas
+    checked = 0
+    for s in _steps(w):
+        dev.grads_into(s, grads)
+        a.step(grads, w.lr)
+        b.step(grads, w.lr)
+        ma = a.sync()
+        mb, stats = b.sync_stats()
+        g = synth.host_grad_rows(w, s)
+        oracle.local_step(ocfg, ost, g, s, w.lr, 0.0, None)
+        ostats = oracle.sync_stats(ocfg, ost, oracle.schedule(ocfg, s))
+        assert ma == mb == oracle.schedule(ocfg, s)
+        for sid, want_row in ostats.items():
+            got = np.concatenate([stats[sid][:3], stats[sid][4:4 + K], stats[sid][20:20 + K]])
+            want = np.concatenate([want_row[:3], want_row[4:4 + K], want_row[4 + K:4 + 2 * K]])
+            scale = np.maximum(np.abs(want), np.abs(want).max() * 1e-6)
+            err = np.max(np.abs(got - want) / scale)
+            assert err <= 1e-5, (s, sid, err)
+            checked += 1
+    torch.cuda.synchronize()
+    assert checked >= 6
+    for p, q in zip(a.states(), b.states()):
+        assert torch.equal(p, q)
+    a.close()
+    b.close()
+    torch.cuda.empty_cache()
+
+
 @pytest.mark.parametrize("fused", [False, True], ids=["separate", "fused"])
 def test_outer_nesterov_single_replica(fused):
     """K = 1: averaging is the identity, but the Nesterov outer step still
