@@ -532,22 +532,25 @@ def test_outer_nesterov_full_size_bench_workload():
 # ------------------------------------------------------------ averaging diagnostics
 
 
-def _stats_case(name, outer=None, steps=None):
-    w = synth.small_variant(synth.WORKLOADS[name], 50_000, tail=8)
+def _stats_case(name, outer=None, steps=None, tail=8):
+    w = synth.small_variant(synth.WORKLOADS[name], 50_000, tail=tail)
     w = w.replace(replicas=min(w.replicas, 16), steps=steps or w.steps)
     return w
 
 
-@pytest.mark.parametrize("name,outer", [("adam_n3_k4_p16m", None), ("adopt_n2_k8_p124m_bf16", None),
-                                        ("sgdm_n2_k16_p354m_clip", None), ("adam_n3_k4_p16m", (0.7, 0.9)),
-                                        ("adopt_n2_k8_p124m_bf16", (0.7, 0.9))],
-                         ids=["adam", "adopt_bf16", "sgdm_k16", "adam_nesterov", "adopt_bf16_nesterov"])
-def test_sync_stats_against_oracle(name, outer):
+@pytest.mark.parametrize("name,outer,tail", [("adam_n3_k4_p16m", None, 8), ("adopt_n2_k8_p124m_bf16", None, 8),
+                                             ("sgdm_n2_k16_p354m_clip", None, 8), ("adam_n3_k4_p16m", (0.7, 0.9), 8),
+                                             ("adopt_n2_k8_p124m_bf16", (0.7, 0.9), 8), ("adam_n3_k4_p16m", None, 37),
+                                             ("adopt_n2_k8_p124m_bf16", (0.7, 0.9), 37)],
+                         ids=["adam", "adopt_bf16", "sgdm_k16", "adam_nesterov", "adopt_bf16_nesterov", "adam_odd",
+                              "adopt_bf16_nesterov_odd"])
+def test_sync_stats_against_oracle(name, outer, tail):
     """mtdao_sync_stats: averaged states bit-identical to mtdao_sync, and the
     diagnostics of every averaged state equal the oracle's on the same
     pre-average values (fp32: 1e-5 relative; bf16 x: rounding flips of x
-    shift the worker differences by a bf16 ulp, bound 2e-3)."""
-    w = _stats_case(name)
+    shift the worker differences by a bf16 ulp, bound 2e-3).  An odd tail
+    takes the one-element-per-lane path."""
+    w = _stats_case(name, tail=tail)
     w = w.replace(period_x=4, period_u=(6,) * w.n_moments, period_v=8, steps=24)
     log(f"case stats {w.name} K={w.replicas} outer={outer}")
     d = torch.device("cuda:0")
