@@ -28,12 +28,24 @@ def _steps(w, start=0):
     return list(range(start + 1, w.steps + 1))
 
 
+def _aligned_tail(name: str, target: int, tail: int) -> int:
+    """A tail of at least ``tail`` elements that makes the row length a
+    multiple of 8 (16-byte slots for fp32 and bf16 rows) when ``tail`` is
+    even, and odd (the one-element path) when ``tail`` is odd."""
+    base = synth.small_variant(synth.WORKLOADS[name], target).numel
+    if tail % 2:
+        return tail + (base + tail + 1) % 2
+    return tail + (-(base + tail)) % 8
+
+
 @pytest.mark.parametrize("tail", [40, 37], ids=["aligned_tail", "odd_tail"])
 @pytest.mark.parametrize("name", NAMES)
 def test_small_variant_full_compare(name, tail):
     """~60k elements per replica (tens of tiles) plus a ragged tail; the
-    odd tail takes the scalar path of every kernel."""
-    w = synth.small_variant(synth.WORKLOADS[name], 60_000, tail=tail)
+    aligned tail makes the row length a multiple of 8 (the 16-byte slots of
+    every kernel), the odd tail takes the one-element path."""
+    w = synth.small_variant(synth.WORKLOADS[name], 60_000, tail=_aligned_tail(name, 60_000, tail))
+    assert w.numel % 8 == 0 if tail % 2 == 0 else w.numel % 2 == 1
     log(f"case small {w.name} P={w.numel} K={w.replicas} T={w.steps}")
     g = run_gpu(w, _steps(w))
     o = run_oracle(w, _steps(w))
@@ -301,7 +313,7 @@ def _run_fused(w, steps, start_step=0, masks=None, dev=None):
 def test_step_sync_bit_identical_to_separate_calls(name, tail):
     """mtdao_step_sync (one fused pass) == mtdao_local_step + mtdao_sync, bit
     for bit, over every workload's full step sequence."""
-    w = synth.small_variant(synth.WORKLOADS[name], 60_000, tail=tail)
+    w = synth.small_variant(synth.WORKLOADS[name], 60_000, tail=_aligned_tail(name, 60_000, tail))
     log(f"case fused {w.name} P={w.numel} K={w.replicas}")
     sep = run_gpu(w, _steps(w))
     fused, applied = _run_fused(w, _steps(w))
@@ -394,7 +406,8 @@ def _run_prob_gpu(w, steps, masks, dev=None):
     dev = dev or DeviceInputs(w, d)
     cfg = abi.config_from_workload(w, sync_order=abi.MTDAO_SYNC_MOMENTA_IN_STEP)
     opt = MtdaoOptimizer(cfg, d, x0=dev.x0_row())
-    grads = torch.empty((w.replicas, w.numel), dtype=torch.float32, device=d)
+    gdt = torch.bfloat16 if w.grad_dtype == "bf16" else torch.float32
+    grads = torch.empty((w.replicas, w.numel), dtype=gdt, device=d)
     applied = []
     for s, m in zip(steps, masks):
         dev.grads_into(s, grads)
@@ -410,13 +423,15 @@ def _prob_workload(name, **kw):
     return w if name == "full" else synth.small_variant(w, 60_000, tail=37 if name == "odd" else 40)
 
 
-@pytest.mark.parametrize("size", ["aligned", "odd", "full", "k17"])
+@pytest.mark.parametrize("size", ["aligned", "odd", "full", "k17", "bf16"])
 def test_probabilistic_sync_against_oracle(size):
     """Bernoulli averaging events (p_x = 1/16, p_u = 1/4, 1/32; drawn on the
     host) through mtdao_step_sync with the averaged-momenta order, against
     the oracle's Algorithm 4 on the same events.  K = 16 runs the
-    wave-per-replica kernel, K = 17 the thread-per-column one."""
-    w = _prob_workload(size, steps=40 if size == "full" else 64, **({"replicas": 17} if size == "k17" else {}))
+    wave-per-replica kernel, K = 17 the thread-per-column one; "bf16" takes
+    bf16 parameters and gradients."""
+    extra = {"k17": {"replicas": 17}, "bf16": {"param_dtype": "bf16", "grad_dtype": "bf16"}}.get(size, {})
+    w = _prob_workload(size, steps=40 if size == "full" else 64, **extra)
     masks = synth.bernoulli_masks(123, w.steps, 2, 1 / 16, (1 / 4, 1 / 32))
     assert any(m & 0b010 for m in masks) and any(m & 1 for m in masks)
     log(f"case prob {size} P={w.numel} K={w.replicas} masks={sum(1 for m in masks if m)}")
