@@ -227,7 +227,8 @@ struct StepParams {
   float* v;                // [K][P] second moment (Adam, ADOPT)
   const float* scale;      // [K] global-norm clip factors, or nullptr
   int64_t P;               // row length
-  int64_t tiles;           // ceil(P / (B * V * U)): tiles of one row
+  int64_t tiles;           // tiles of one row (all windows)
+  int64_t wlen;            // k_local_step with NW = 2: elements of the first window
   float beta[kMaxN];       // beta_{1,j}
   float omb[kMaxN];        // 1 - beta_{1,j}
   float w[kMaxN];          // omega_j (times 1/(1 - beta_{1,j}^s) for bias-corrected Adam)
@@ -298,7 +299,12 @@ __device__ __forceinline__ void update_element(const StepParams& p, float sc, fl
 //   ORDER      ADOPT normalisation order (kPrev: v from before this step)
 //   B          threads per block
 //   C          elements per piece of the tile -> element map (tile_elem)
-template <int FORM, int N, typename XT, typename GT, int V, int U, int NTM, int ORDER, int B = kBlock, int C = 0>
+//   NW         windows of the row processed at once: with NW = 2 groups of
+//              8 workgroups take, in turn, tiles of [0, wlen) and of
+//              [wlen, P), so each stream is read at two places half a row
+//              apart
+template <int FORM, int N, typename XT, typename GT, int V, int U, int NTM, int ORDER, int B = kBlock, int C = 0,
+          int NW = 1>
 __global__ __launch_bounds__(B) void k_local_step(StepParams p) {
   constexpr bool NTL = (NTM & 1) != 0, NTS = (NTM & 2) != 0;
   const int64_t m = blockIdx.y;
@@ -312,12 +318,16 @@ __global__ __launch_bounds__(B) void k_local_step(StepParams p) {
   const float sc = (FORM != kAdopt && p.scale != nullptr) ? p.scale[m] : 1.0f;
 
   for (int64_t tile = blockIdx.x; tile < p.tiles; tile += gridDim.x) {
+    // window of this tile: [base, end) of the row (even and odd workgroups)
+    const int64_t w = NW == 1 ? 0 : (tile & 1);
+    const int64_t wt = NW == 1 ? tile : (tile >> 1);
+    const int64_t base = w * p.wlen, end = NW == 1 ? p.P : (w == 0 ? p.wlen : p.P);
     float gv[U][V], xv[U][V], uv[U][N][V], vv[U][V];
     // issue every load of the tile before any arithmetic
 #pragma unroll
     for (int k = 0; k < U; ++k) {
-      const int64_t e = tile_elem<B * V * U, C>(tile, (k * B + (int)threadIdx.x) * V);
-      if (e < p.P) {
+      const int64_t e = base + tile_elem<B * V * U, C>(wt, (k * B + (int)threadIdx.x) * V);
+      if (e < end) {
         load_v<GT, V, NTL>(g, e, gv[k]);
         load_v<XT, V, NTL>(x, e, xv[k]);
 #pragma unroll
@@ -327,8 +337,8 @@ __global__ __launch_bounds__(B) void k_local_step(StepParams p) {
     }
 #pragma unroll
     for (int k = 0; k < U; ++k) {
-      const int64_t e = tile_elem<B * V * U, C>(tile, (k * B + (int)threadIdx.x) * V);
-      if (e >= p.P) continue;
+      const int64_t e = base + tile_elem<B * V * U, C>(wt, (k * B + (int)threadIdx.x) * V);
+      if (e >= end) continue;
 #pragma unroll
       for (int t = 0; t < V; ++t) {
         float uu[N];

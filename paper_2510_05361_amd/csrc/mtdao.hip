@@ -229,18 +229,21 @@ void launch_step(const mtdao_config& c, StepParams p, int V, hipStream_t st) {
     constexpr int FORM = decltype(form)::value, N = decltype(n)::value, VV = decltype(vw)::value;
     using XT = typename decltype(xt)::type;
     using GT = typename decltype(gt)::type;
-    constexpr int U = step_slots(FORM), C = piece_for(VV);
-    p.tiles = tiles_for<kBlock * VV * U, C>(p.P);
+    constexpr int U = step_slots(FORM), C = piece_for(VV), T = kBlock * VV * U;
+    // two windows of whole tiles: [0, wlen) and [wlen, P)
+    p.wlen = ((p.P + 1) / 2 + T - 1) / T * T;
+    if (p.wlen > p.P) p.wlen = p.P;
+    p.tiles = 2 * tiles_for<T, C>(p.wlen);
     const dim3 grid = grid_for(p.tiles, c.replicas);
     if constexpr (FORM == kAdopt) {
       if (c.adopt_order == MTDAO_ADOPT_CUR) {
-        hipLaunchKernelGGL((k_local_step<FORM, N, XT, GT, VV, U, kStepNT, kCur, kBlock, C>), grid, dim3(kBlock), 0,
+        hipLaunchKernelGGL((k_local_step<FORM, N, XT, GT, VV, U, kStepNT, kCur, kBlock, C, 2>), grid, dim3(kBlock), 0,
                            st, p);
         return;
       }
     }
-    hipLaunchKernelGGL((k_local_step<FORM, N, XT, GT, VV, U, kStepNT, kPrev, kBlock, C>), grid, dim3(kBlock), 0, st,
-                       p);
+    hipLaunchKernelGGL((k_local_step<FORM, N, XT, GT, VV, U, kStepNT, kPrev, kBlock, C, 2>), grid, dim3(kBlock), 0,
+                       st, p);
   });
 }
 
