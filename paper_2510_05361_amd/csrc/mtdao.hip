@@ -230,20 +230,32 @@ void launch_step(const mtdao_config& c, StepParams p, int V, hipStream_t st) {
     using XT = typename decltype(xt)::type;
     using GT = typename decltype(gt)::type;
     constexpr int U = step_slots(FORM), C = piece_for(VV), T = kBlock * VV * U;
-    // two windows of whole tiles: [0, wlen) and [wlen, P)
-    p.wlen = ((p.P + 1) / 2 + T - 1) / T * T;
-    if (p.wlen > p.P) p.wlen = p.P;
-    p.tiles = 2 * tiles_for<T, C>(p.wlen);
-    const dim3 grid = grid_for(p.tiles, c.replicas);
-    if constexpr (FORM == kAdopt) {
-      if (c.adopt_order == MTDAO_ADOPT_CUR) {
-        hipLaunchKernelGGL((k_local_step<FORM, N, XT, GT, VV, U, kStepNT, kCur, kBlock, C, 2>), grid, dim3(kBlock), 0,
-                           st, p);
-        return;
+    // every stream read at two places at once: rows m and m + ceil(K/2)
+    // when K > 1, else the two halves [0, wlen) and [wlen, P) of the row
+    auto go = [&](auto win) {
+      constexpr int WIN = decltype(win)::value;
+      dim3 grid;
+      if constexpr (WIN == kWinPairs) {
+        p.tiles = 2 * tiles_for<T, C>(p.P);
+        grid = grid_for(p.tiles, (c.replicas + 1) / 2);
+      } else {
+        p.wlen = ((p.P + 1) / 2 + T - 1) / T * T;
+        if (p.wlen > p.P) p.wlen = p.P;
+        p.tiles = 2 * tiles_for<T, C>(p.wlen);
+        grid = grid_for(p.tiles, c.replicas);
       }
-    }
-    hipLaunchKernelGGL((k_local_step<FORM, N, XT, GT, VV, U, kStepNT, kPrev, kBlock, C, 2>), grid, dim3(kBlock), 0,
-                       st, p);
+      if constexpr (FORM == kAdopt) {
+        if (c.adopt_order == MTDAO_ADOPT_CUR) {
+          hipLaunchKernelGGL((k_local_step<FORM, N, XT, GT, VV, U, kStepNT, kCur, kBlock, C, WIN>), grid, dim3(kBlock),
+                             0, st, p);
+          return;
+        }
+      }
+      hipLaunchKernelGGL((k_local_step<FORM, N, XT, GT, VV, U, kStepNT, kPrev, kBlock, C, WIN>), grid, dim3(kBlock), 0,
+                         st, p);
+    };
+    if (c.replicas > 1) go(IntC<kWinPairs>{});
+    else go(IntC<kWinHalves>{});
   });
 }
 
@@ -594,6 +606,7 @@ StepParams prepare_step(mtdao_handle* h, const void* grads, float lr, float adop
   for (int j = 0; j < c.n_moments; ++j) p.u[j] = h->u[j];
   p.v = h->v;
   p.P = P;
+  p.replicas = c.replicas;
   double wsum = 0.0;
   const bool bc = c.form == MTDAO_ADAM && c.bias_correction;
   for (int j = 0; j < c.n_moments; ++j) {
