@@ -909,10 +909,37 @@ __global__ __launch_bounds__(64 * kWaveMaxK) void k_replica_mean_waves(MeanParam
 
 // ----------------------------------------------------- global-norm clip
 
+// One 64-lane DPP move of a double (both halves), rows outside RowMask and
+// lanes without a source read 0.
+template <int Ctrl, int RowMask>
+__device__ __forceinline__ double dpp_f64(double v) {
+  const unsigned long long b = __builtin_bit_cast(unsigned long long, v);
+  const int lo = __builtin_amdgcn_update_dpp(0, (int)(unsigned)b, Ctrl, RowMask, 0xf, true);
+  const int hi = __builtin_amdgcn_update_dpp(0, (int)(unsigned)(b >> 32), Ctrl, RowMask, 0xf, true);
+  return __builtin_bit_cast(double, ((unsigned long long)(unsigned)hi << 32) | (unsigned)lo);
+}
+
+// Sum of a double over the 64 lanes of a wave, in a fixed order, returned
+// as a wave-uniform value.  Quad permutes [1,0,3,2] and [2,3,0,1], the
+// half-row mirror and the row mirror leave every lane with its 16-lane
+// row's sum; the row-15 broadcast (rows 1 and 3) and the row-31 broadcast
+// (rows 2 and 3) carry the lower rows' sums into row 3, and lane 63 holds
+// the total.  DPP moves stay in the vector ALU: the xor-shuffle butterfly
+// goes through ds_bpermute, two LDS permutes of 256 B per step for a
+// double, and in the diagnostics kernel, which ends every workgroup with
+// five such sums per wave, that LDS traffic cost more time than the
+// workgroup's own data exchange.
 __device__ __forceinline__ double wave_sum(double a) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) a += __shfl_xor(a, o, 64);
-  return a;
+  a += dpp_f64<0xB1, 0xf>(a);   // quad_perm [1,0,3,2]
+  a += dpp_f64<0x4E, 0xf>(a);   // quad_perm [2,3,0,1]
+  a += dpp_f64<0x141, 0xf>(a);  // row_half_mirror
+  a += dpp_f64<0x140, 0xf>(a);  // row_mirror
+  a += dpp_f64<0x142, 0xa>(a);  // row_bcast:15 into rows 1, 3
+  a += dpp_f64<0x143, 0xc>(a);  // row_bcast:31 into rows 2, 3
+  const unsigned long long b = __builtin_bit_cast(unsigned long long, a);
+  const unsigned lo = __builtin_amdgcn_readlane((int)(unsigned)b, 63);
+  const unsigned hi = __builtin_amdgcn_readlane((int)(unsigned)(b >> 32), 63);
+  return __builtin_bit_cast(double, ((unsigned long long)hi << 32) | lo);
 }
 
 // Partial sums of g^2 in fp64 for replica blockIdx.y; each block writes
@@ -1020,8 +1047,11 @@ constexpr int kStatsStride = 4 + 2 * kStatsMaxK;  // doubles per state (layout i
 // and as workgroups are dispatched in order the pieces in flight stay a
 // compact window, as in the plain mean (a fixed grid of workgroups
 // striding over the row scattered them and ran 30% slower).  Each wave
-// keeps fp64 sums for its own replica (wave 0 also those of cbar and xo)
-// and the workgroup writes its kStatsSums(K) sums, contiguous, to
+// keeps fp64 sums for its own replica (wave 0 also those of cbar and xo):
+// a lane forms the V products of a piece in fp32 (one rounding each, about
+// 6e-8 relative) and adds their fp32 sum to the fp64 sums, which keeps the
+// fp64 work per element to a fraction of an operation.  The workgroup
+// writes its kStatsSums(K) sums, contiguous, to
 // partials[state][workgroup][sum]:
 //   0 ||cbar||^2, 1 sum_m ||c^m - cbar||^2, 2 ||xo||^2,
 //   3 + m ||c^m||^2, 3 + K + m <c^m, cbar>.
@@ -1074,17 +1104,27 @@ __global__ __launch_bounds__(64 * kStatsMaxK) void k_replica_mean_stats(MeanPara
 #pragma unroll
       for (int t = 0; t < V; ++t) out[t] = outer ? lds_stats[t * 64 + lane] : mean[t];
       store_v<T, V, true>(row, e, out);
+      // the piece's V terms in fp32, added to the fp64 sums once per piece
+      float f_sq = 0.0f, f_dot = 0.0f, f_var = 0.0f, f_mean = 0.0f, f_ref = 0.0f;
 #pragma unroll
       for (int t = 0; t < V; ++t) {
-        const double cbar = outer ? (double)xo[t] - (double)mean[t] : (double)mean[t];
-        const double c = outer ? (double)xo[t] - (double)a[t] : (double)a[t];
-        a_sq += c * c;
-        a_dot += c * cbar;
-        a_var += (c - cbar) * (c - cbar);
+        const float cbar = outer ? xo[t] - mean[t] : mean[t];
+        const float c = outer ? xo[t] - a[t] : a[t];
+        const float dv = a[t] - mean[t];  // c - cbar up to sign
+        f_sq = __builtin_fmaf(c, c, f_sq);
+        f_dot = __builtin_fmaf(c, cbar, f_dot);
+        f_var = __builtin_fmaf(dv, dv, f_var);
         if (m == 0) {
-          a_mean += cbar * cbar;
-          if (outer) a_ref += (double)xo[t] * (double)xo[t];
+          f_mean = __builtin_fmaf(cbar, cbar, f_mean);
+          if (outer) f_ref = __builtin_fmaf(xo[t], xo[t], f_ref);
         }
+      }
+      a_sq += (double)f_sq;
+      a_dot += (double)f_dot;
+      a_var += (double)f_var;
+      if (m == 0) {
+        a_mean += (double)f_mean;
+        if (outer) a_ref += (double)f_ref;
       }
     }
     __syncthreads();
