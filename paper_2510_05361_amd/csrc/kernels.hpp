@@ -857,37 +857,47 @@ __global__ __launch_bounds__(kBlock) void k_replica_mean(MeanParams p) {
   }
 }
 
-// The same mean with one wavefront per replica (blockDim = 64 K,
-// 1 < K <= kWaveMaxK; dynamic LDS of K * 64 * V floats): each workgroup
-// takes one piece of 64 V consecutive elements (a 1 KiB access for fp32 and
-// bf16 rows), wave m loads row m's piece, the K pieces meet in LDS, column t
-// of the piece is averaged by wave t mod K with mean_add / mean_of in
-// replica order (so every element gets exactly the value k_replica_mean
-// gives), the OuterOpt runs element by element on x, and every wave stores
-// the mean to its own row.  Each wave then issues one load and one store
-// per piece, as a plain copy does; a thread that walks all K rows of its
-// columns (k_replica_mean) ran the K = 4 mean at 74% of the HBM peak on
-// MI355X, this kernel at 82.6%.  Barriers are reached by every thread, also
-// in the row tail.
-template <typename T, int V, bool NT>
-__global__ __launch_bounds__(64 * kWaveMaxK) void k_replica_mean_waves(MeanParams p) {
+// The same mean with whole waves per replica row (blockDim = 64 K / R,
+// 1 < K <= kWaveMaxK, R | K; dynamic LDS of K * 64 * V floats): each
+// workgroup takes one piece of 64 V consecutive elements (a 1 KiB access
+// for fp32 and bf16 rows), wave w loads the pieces of rows w, w + W, ...,
+// w + (R - 1) W (W = K / R waves), the K pieces meet in LDS, column t of
+// the piece is averaged by wave t mod W with mean_add / mean_of in replica
+// order (so every element gets exactly the value k_replica_mean gives),
+// the OuterOpt runs element by element on x, and each wave stores the mean
+// to its rows.  Each wave then issues R loads and R stores per piece, as a
+// plain copy does; a thread that walks all K rows of its columns
+// (k_replica_mean) ran the K = 4 mean at 74% of the HBM peak on MI355X,
+// this kernel at 82.6%.  With K = 16 and one row per wave only two
+// 16-wave workgroups fit on a CU and every barrier idles 16 waves; two rows
+// per wave took the K = 16 mean from 8.2 to 7.6 ms (69% to 74.5%) and the
+// K = 8 bf16 mean from 0.745 to 0.685 ms, four rows per wave gave nothing.
+// Barriers are reached by every thread, also in the row tail.
+template <typename T, int V, bool NT, int R = 1>
+__global__ __launch_bounds__(64 * kWaveMaxK / R) void k_replica_mean_waves(MeanParams p) {
   extern __shared__ float lds_mean[];  // [K][64 V]
   T* __restrict__ s = reinterpret_cast<T*>(p.state[blockIdx.y]);
-  const int32_t K = p.K, m = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int32_t K = p.K, W = K / R, w = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const double rk = 1.0 / (double)K;
   const bool outer = (int32_t)blockIdx.y == p.outer_state;
-  T* __restrict__ row = s + (int64_t)m * p.P;
   for (int64_t tile = blockIdx.x; tile < p.tiles; tile += gridDim.x) {
     const int64_t e = tile * (int64_t)(64 * V) + (int64_t)lane * V;
     const bool in = e < p.P;
-    float a[V];
+    float a[R][V];
 #pragma unroll
-    for (int t = 0; t < V; ++t) a[t] = 0.0f;
-    if (in) load_v<T, V, NT>(row, e, a);
+    for (int r = 0; r < R; ++r)
 #pragma unroll
-    for (int t = 0; t < V; ++t) lds_mean[(m * V + t) * 64 + lane] = a[t];
+      for (int t = 0; t < V; ++t) a[r][t] = 0.0f;
+    if (in) {
+#pragma unroll
+      for (int r = 0; r < R; ++r) load_v<T, V, NT>(s + (int64_t)(w + r * W) * p.P, e, a[r]);
+    }
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+#pragma unroll
+      for (int t = 0; t < V; ++t) lds_mean[((w + r * W) * V + t) * 64 + lane] = a[r][t];
     __syncthreads();
-    for (int t = m; in && t < V; t += K) {
+    for (int t = w; in && t < V; t += W) {
       const float s0 = lds_mean[t * 64 + lane];
       double d = 0.0;
       for (int32_t q = 1; q < K; ++q) mean_add(d, lds_mean[(q * V + t) * 64 + lane], s0);
@@ -895,13 +905,15 @@ __global__ __launch_bounds__(64 * kWaveMaxK) void k_replica_mean_waves(MeanParam
     }
     __syncthreads();
     if (outer) {
-      outer_step_piece<V>(p.outer, tile * (int64_t)(64 * V), p.P, K, m, lane, lds_mean);
+      outer_step_piece<V>(p.outer, tile * (int64_t)(64 * V), p.P, W, w, lane, lds_mean);
       __syncthreads();
     }
     if (in) {
+      float b[V];
 #pragma unroll
-      for (int t = 0; t < V; ++t) a[t] = lds_mean[t * 64 + lane];
-      store_v<T, V, NT>(row, e, a);
+      for (int t = 0; t < V; ++t) b[t] = lds_mean[t * 64 + lane];
+#pragma unroll
+      for (int r = 0; r < R; ++r) store_v<T, V, NT>(s + (int64_t)(w + r * W) * p.P, e, b);
     }
     __syncthreads();
   }

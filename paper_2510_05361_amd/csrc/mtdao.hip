@@ -326,13 +326,20 @@ template <typename T>
 void launch_mean(MeanParams p, int nstates, int V, hipStream_t st) {
   constexpr int VW = sizeof(T) == 2 ? 8 : 4;  // elements of a 16-byte slot
   if (p.K > 1 && p.K <= kWaveMaxK) {
-    // one wavefront per replica, one piece of 64 V elements per workgroup
+    // one piece of 64 V elements per workgroup; one wavefront per replica,
+    // or per two replicas for even K >= 8
     const int vw = V == 1 ? 1 : VW;
     p.tiles = (p.P + 64 * vw - 1) / (64 * vw);
-    const dim3 grid = grid_for(p.tiles, nstates), block(64 * p.K);
+    const bool two = p.K >= 8 && p.K % 2 == 0;
+    const dim3 grid = grid_for(p.tiles, nstates), block(64 * (two ? p.K / 2 : p.K));
     const size_t lds = (size_t)p.K * 64 * vw * sizeof(float);
-    if (vw == 1) hipLaunchKernelGGL((k_replica_mean_waves<T, 1, kMeanNT>), grid, block, lds, st, p);
-    else hipLaunchKernelGGL((k_replica_mean_waves<T, VW, kMeanNT>), grid, block, lds, st, p);
+    if (two) {
+      if (vw == 1) hipLaunchKernelGGL((k_replica_mean_waves<T, 1, kMeanNT, 2>), grid, block, lds, st, p);
+      else hipLaunchKernelGGL((k_replica_mean_waves<T, VW, kMeanNT, 2>), grid, block, lds, st, p);
+    } else {
+      if (vw == 1) hipLaunchKernelGGL((k_replica_mean_waves<T, 1, kMeanNT>), grid, block, lds, st, p);
+      else hipLaunchKernelGGL((k_replica_mean_waves<T, VW, kMeanNT>), grid, block, lds, st, p);
+    }
     return;
   }
   // K = 1 (an outer step only) and K > kWaveMaxK: one thread per column
@@ -354,8 +361,9 @@ void launch_mean(MeanParams p, int nstates, int V, hipStream_t st) {
 // nstates * kStatsSums(K) * (workgroups + chunks) doubles.
 //
 // Pieces per workgroup, measured on MI355X at 1.31B params x 4 replicas
-// (one state): 1 -> 14.5 ms (the workgroup's closing reduction dominates),
-// 4 -> 7.5 ms, 16 -> 7.7 ms, 64 -> 8.0 ms, 1024 -> 8.4 ms.
+// (one state, DPP wave sums): 2 -> 7.65 ms, 3 -> 7.3 ms, 4 -> 6.9 ms,
+// 6 -> 7.35 ms, 8 -> 7.3 ms.  With shuffle-based wave sums the closing
+// reduction of each workgroup dominated below 4 (1 -> 14.5 ms, 2 -> 9.5 ms).
 constexpr int32_t kStatsPieces = 4;
 int64_t stats_pieces(int64_t P, int V) { return (P + 64 * V - 1) / (64 * V); }
 int64_t stats_blocks(int64_t pieces) { return (pieces + 8 * kStatsPieces - 1) / (8 * kStatsPieces) * 8; }
