@@ -227,6 +227,34 @@ def test_sync_idempotent_and_explicit_masks():
     free(g)
 
 
+@pytest.mark.parametrize("tail", [40, 37], ids=["aligned_tail", "odd_tail"])
+@pytest.mark.parametrize("base,K", [("adam_n3_k4_p16m", 6), ("adam_n3_k4_p16m", 10), ("adopt_n2_k8_p124m_bf16", 12),
+                                    ("adam_n3_k4_p16m", 14), ("adopt_n2_k8_p124m_bf16", 10)],
+                         ids=["fp32_k6", "fp32_k10", "bf16x_k12", "fp32_k14", "bf16x_k10"])
+def test_mean_wave_shapes(base, K, tail):
+    """The replica mean with one row per wave (K = 6) and two rows per wave
+    (even K >= 8: 5 to 7 waves, so the column-to-wave assignment wraps for
+    the 4 fp32 and 8 bf16 columns of a lane) against the oracle on every
+    element, and bit-identical to the diagnostics pass, which averages with
+    one wave per row."""
+    w = synth.small_variant(synth.WORKLOADS[base], 20_000, tail=_aligned_tail(base, 20_000, tail))
+    w = w.replace(replicas=K, steps=3, period_x=0, period_u=(0,) * w.n_moments, period_v=0)
+    log(f"case mean shapes {w.name} P={w.numel} K={K}")
+    a = run_gpu(w, _steps(w))
+    b = run_gpu(w, _steps(w))
+    o = run_oracle(w, _steps(w))
+    full = (1 << (w.n_moments + 2)) - 1
+    assert a.opt.sync(full) == full
+    mb, _ = b.opt.sync_stats(full)
+    assert mb == full
+    oracle.sync(oracle.OracleConfig.from_workload(w), o.state, full)
+    torch.cuda.synchronize()
+    for p, q in zip(a.opt.states(), b.opt.states()):
+        assert torch.equal(p, q)
+    compare(w, a.opt, o, f"mean-K{K}")
+    free(a, b)
+
+
 def test_deterministic():
     """Two runs of the clipped SGDM workload are bit-identical (fixed-order
     norm reduction, no atomics)."""
