@@ -9,7 +9,10 @@
  * with Local Updates", Section 2.3 Algorithm 1 = Adam form, Appendix
  * Algorithm 2 = ADOPT form, Appendix Algorithm 3 = SGDM form):
  *   one local step of every worker m for every element i, followed, at
- *   the caller's request, by the replica mean E_m[.] of one state.
+ *   the caller's request, by the replica mean E_m[.] of one state; also
+ *   the step of the probabilistic SGDM variant (Algorithm 4), the Nesterov
+ *   OuterOpt at an averaging event of x, and the averaging diagnostics of
+ *   one state (Section 4.1's metrics).
  * Arithmetic is IEEE double throughout.  Each state store rounds once to
  * its storage type (fp32 and bf16 with round-to-nearest-even, or fp64),
  * which puts the rounding points where a device kernel stores them.
@@ -31,7 +34,8 @@
  *    published ADOPT order: step 1 only sets v = g^2); the literal order of
  *    Algorithm 2 (normalise by the freshly updated v) is the "current"
  *    variant; clip(., c_t) is an element-wise clamp to [-c_t, c_t];
- *  - OuterOpt is the plain arithmetic mean.
+ *  - OuterOpt is the plain arithmetic mean unless the Nesterov OuterOpt is
+ *    asked for (its reading is given where it is defined below).
  */
 #include <math.h>
 #include <stdint.h>
