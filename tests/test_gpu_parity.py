@@ -720,3 +720,56 @@ def test_degenerate_sizes(P, K, form):
     for p, q in zip(g.opt.states(), f.opt.states()):
         assert torch.equal(p, q)
     free(g, f)
+
+
+# ------------------------------------------------------------ seeded random configurations
+
+def _random_workload(seed: int):
+    """A small configuration drawn from seed: form, N, betas, omegas (the
+    gradient weight 1 - sum omega sometimes exactly 0), K (1 to 17), storage
+    types, ADOPT order, bias correction, clip, periods (0 = never, 1 =
+    every step) and a ragged row tail."""
+    rng = np.random.Generator(np.random.PCG64(9000 + seed))
+    form = ["adam", "adopt", "sgdm"][seed % 3]
+    base = {"adam": "adam_n3_k4_p16m", "adopt": "adopt_n2_k8_p124m_bf16", "sgdm": "sgdm_n2_k16_p354m_clip"}[form]
+    n = int(rng.integers(1, 5))
+    beta1 = tuple(float(b) for b in np.sort(rng.choice([0.0, 0.5, 0.9, 0.95, 0.99, 0.995, 0.999], n, replace=False)))
+    total = 1.0 if rng.random() < 0.25 else float(rng.uniform(0.3, 0.95))
+    wts = rng.uniform(0.1, 1.0, n)
+    omega = tuple(float(np.float32(total * x / wts.sum())) for x in wts)
+    periods = [0, 1, 2, 3, 5]
+    kw = dict(replicas=int(rng.choice([1, 2, 3, 5, 8, 12, 16, 17])), beta1=beta1, omega=omega, steps=12,
+              param_dtype=str(rng.choice(["f32", "bf16"])), grad_dtype=str(rng.choice(["f32", "bf16"])),
+              period_x=int(rng.choice(periods)), period_u=tuple(int(rng.choice(periods)) for _ in range(n)),
+              period_v=int(rng.choice(periods)), start_step=0)
+    if form == "adopt":
+        kw.update(adopt_order=str(rng.choice(["prev", "cur"])), clip_rho=0.0)
+    else:
+        kw.update(clip_rho=float(rng.choice([0.0, 1.0])))
+    if form == "adam":
+        kw.update(bias_correction=bool(rng.random() < 0.7))
+    kw.pop("start_step")
+    tail = int(rng.choice([0, 1, 7, 37, 40]))
+    w = synth.small_variant(synth.WORKLOADS[base], int(rng.integers(3_000, 20_000)), tail=tail)
+    fused = bool(rng.random() < 0.5)
+    outer = None
+    if kw["period_x"] > 0 and rng.random() < 0.3:
+        # lr (1 + mu) / (1 - mu) <= 15.2 stays within the bf16 outer bound
+        outer = (float(np.float32(rng.uniform(0.5, 0.8))), float(np.float32(rng.choice([0.0, 0.5, 0.9]))))
+    return w.replace(**kw), fused, outer
+
+
+@pytest.mark.parametrize("seed", range(48))
+def test_random_configs(seed):
+    """Seeded random small configurations (some with the Nesterov OuterOpt)
+    through the separate or the fused entry points, every element against
+    the oracle and the applied masks bit for bit."""
+    w, fused, outer = _random_workload(seed)
+    log(f"case random {seed} {w.form} N={w.n_moments} K={w.replicas} P={w.numel} x={w.param_dtype} "
+        f"g={w.grad_dtype} periods={w.period_x}/{w.period_u}/{w.period_v} clip={w.clip_rho} fused={fused} "
+        f"outer={outer}")
+    g = run_gpu(w, _steps(w), fused=fused, outer=outer)
+    o = run_oracle(w, _steps(w), outer=outer)
+    assert g.masks == o.masks
+    compare(w, g.opt, o, f"random{seed}")
+    free(g)
