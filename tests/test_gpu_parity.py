@@ -773,3 +773,87 @@ def test_random_configs(seed):
     assert g.masks == o.masks
     compare(w, g.opt, o, f"random{seed}")
     free(g)
+
+
+@pytest.mark.parametrize("seed", range(16))
+def test_random_probabilistic(seed):
+    """Algorithm 4 on seeded random SGDM configurations: N, betas (beta_1 = 0
+    in half of them, the gradient as a momentum), omegas, K (2 to 17),
+    storage types, clip, and Bernoulli events with drawn probabilities,
+    through mtdao_step_sync against the oracle's Algorithm 4."""
+    rng = np.random.Generator(np.random.PCG64(7000 + seed))
+    n = int(rng.integers(1, 5))
+    beta1 = tuple(float(b) for b in np.sort(rng.choice([0.5, 0.9, 0.95, 0.99, 0.999], n, replace=False)))
+    if rng.random() < 0.5:
+        beta1 = (0.0,) + beta1[1:]
+    total = 1.0 if rng.random() < 0.5 else float(rng.uniform(0.4, 0.95))
+    wts = rng.uniform(0.1, 1.0, n)
+    omega = tuple(float(np.float32(total * x / wts.sum())) for x in wts)
+    w = synth.small_variant(synth.WORKLOADS["sgdm_n2_k16_p354m_clip"], int(rng.integers(3_000, 20_000)),
+                            tail=int(rng.choice([0, 1, 7, 37, 40])))
+    w = w.replace(replicas=int(rng.choice([2, 3, 5, 8, 12, 16, 17])), beta1=beta1, omega=omega, steps=24,
+                  period_x=0, period_u=(0,) * n, clip_rho=float(rng.choice([0.0, 1.0])),
+                  param_dtype=str(rng.choice(["f32", "bf16"])), grad_dtype=str(rng.choice(["f32", "bf16"])))
+    p_x = float(rng.choice([0.0, 0.1, 0.3]))
+    p_u = tuple(float(rng.choice([0.05, 0.25, 0.5, 1.0])) for _ in range(n))
+    masks = synth.bernoulli_masks(7100 + seed, w.steps, n, p_x, p_u)
+    log(f"case random prob {seed} N={n} K={w.replicas} P={w.numel} x={w.param_dtype} g={w.grad_dtype} "
+        f"beta={beta1} clip={w.clip_rho} events={sum(1 for m in masks if m)}")
+    opt, applied = _run_prob_gpu(w, _steps(w), masks)
+    assert applied == masks
+    ocfg = oracle.OracleConfig.from_workload(w)
+    ost = oracle.new_state(ocfg, synth.host_x0_row(w), w.replicas)
+    oracle.run_probabilistic(ocfg, ost, lambda s: synth.host_grad_rows(w, s), _steps(w),
+                             lambda s: w.lr, lambda s: masks[s - 1])
+    from gpu_harness import OracleResult
+    compare(w, opt, OracleResult(ost, masks, None), f"random-prob{seed}")
+    opt.close()
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("seed", range(16))
+def test_random_sync_stats(seed):
+    """mtdao_sync_stats on seeded random configurations (K up to 16, some
+    with the Nesterov OuterOpt): after a few local steps every state is
+    averaged with its diagnostics; the diagnostics against the oracle's and
+    the averaged states bit-identical to mtdao_sync."""
+    w, _, outer = _random_workload(100 + seed)
+    w = w.replace(replicas=min(w.replicas, 16), steps=5, period_x=0, period_u=(0,) * w.n_moments, period_v=0)
+    log(f"case random stats {seed} {w.form} N={w.n_moments} K={w.replicas} P={w.numel} x={w.param_dtype} "
+        f"outer={outer}")
+    from gpu_harness import gpu_config, oracle_cfg
+    d = torch.device("cuda:0")
+    dev = DeviceInputs(w, d)
+    a = MtdaoOptimizer(gpu_config(w, 0, outer), d, x0=dev.x0_row())
+    b = MtdaoOptimizer(gpu_config(w, 0, outer), d, x0=dev.x0_row())
+    ocfg = oracle_cfg(w, outer)
+    ost = oracle.new_state(ocfg, synth.host_x0_row(w), w.replicas)
+    gdt = torch.bfloat16 if w.grad_dtype == "bf16" else torch.float32
+    grads = torch.empty((w.replicas, w.numel), dtype=gdt, device=d)
+    for s in _steps(w):
+        dev.grads_into(s, grads)
+        a.step(grads, w.lr, w.adopt_clip_value(s))
+        b.step(grads, w.lr, w.adopt_clip_value(s))
+        g = synth.host_grad_rows(w, s)
+        oracle.local_step(ocfg, ost, g, s, w.lr, w.adopt_clip_value(s), oracle.clip_scales(ocfg, g))
+    full = (1 << (w.n_moments + (2 if w.has_v else 1))) - 1
+    assert a.sync(full) == full
+    mb, stats = b.sync_stats(full)
+    assert mb == full
+    ostats = oracle.sync_stats(ocfg, ost, full)
+    K = w.replicas
+    for sid, want_row in ostats.items():
+        got = np.concatenate([stats[sid][:3], stats[sid][4:4 + K], stats[sid][20:20 + K]])
+        want = np.concatenate([want_row[:3], want_row[4:4 + K], want_row[4 + K:4 + 2 * K]])
+        tol = 2e-3 if (sid == 0 and w.param_dtype == "bf16") else 1e-5
+        scale = np.maximum(np.abs(want), np.abs(want).max() * 1e-6)
+        err = np.max(np.abs(got - want) / scale)
+        assert err <= tol, (sid, err, got[:3], want[:3])
+    torch.cuda.synchronize()
+    for p, q in zip(a.states(), b.states()):
+        assert torch.equal(p, q)
+    if outer is not None:
+        assert torch.equal(a.x_outer, b.x_outer) and torch.equal(a.x_outer_mom, b.x_outer_mom)
+    a.close()
+    b.close()
+    torch.cuda.empty_cache()
