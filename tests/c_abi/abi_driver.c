@@ -9,7 +9,13 @@
  *           every averaging event folded into mtdao_step_sync;
  *   case 2: SGDM form (Algorithm 3), N = 2, K = 5, P = 8204, per-worker
  *           global-norm clip rho = 0.05 (active), mtdao_local_step followed
- *           by mtdao_sync on the schedule.
+ *           by mtdao_sync on the schedule;
+ *   case 3: Adam form, N = 2, K = 6, P = 4099, then mtdao_sync_stats of
+ *           every state: the averaging diagnostics (Section 4.1's metrics,
+ *           in the header's MTDAO_STAT_* layout) against the oracle's on
+ *           the same pre-average states, within 1e-5 of
+ *           max(|want|, 1e-6 * the largest statistic of the state).
+ * Every step's mask is also checked against mtdao_schedule (host only).
  * Inputs are seeded splitmix64 fields made here; the driver holds none of
  * the method's arithmetic.  Pass: every applied mask equals the oracle's
  * schedule bit for bit, and every state's max |a - b| / max(|b|, rms(b))
@@ -36,6 +42,7 @@ double oracle_clip_scale(double norm, double rho);
 void oracle_local_step(const oracle_cfg* c, int64_t s, float lr, float clip_c, const double* scale, void* x,
                        void* const* u, void* v, const void* g, int64_t K, int64_t P);
 void oracle_replica_mean(void* state, int32_t dtype, int64_t K, int64_t P);
+void oracle_state_stats(const void* s, int32_t dtype, const float* xo, int64_t K, int64_t P, double* out);
 
 #define CHECK_HIP(call)                                                              \
   do {                                                                               \
@@ -70,7 +77,7 @@ typedef struct {
   int32_t form, K, N;
   int64_t P;
   float beta1[4], omega[4], beta2, eps, rho, lr;
-  int32_t period_x, period_u[4], period_v, steps, fused;
+  int32_t period_x, period_u[4], period_v, steps, fused, stats;
 } drv_case;
 
 static double compare(const float* a, const float* b, int64_t n) {
@@ -184,6 +191,12 @@ static int run_case(const drv_case* t) {
       scale[m] = oracle_clip_scale(sqrt(oracle_sumsq(g + (int64_t)m * P, 0, P)), (double)t->rho);
     oracle_local_step(&oc, s, t->lr, 0.0f, t->rho > 0.0f ? scale : NULL, x, ou, v, g, K, P);
     const uint32_t want = oracle_schedule(s, N, t->period_x, t->period_u, t->period_v, has_v);
+    uint32_t sched = 0;
+    CHECK_MT(NULL, mtdao_schedule(&c, s, &sched));
+    if (sched != want) {
+      fprintf(stderr, "%s: step %d mtdao_schedule 0x%x, oracle 0x%x\n", t->name, s, sched, want);
+      masks_ok = 0;
+    }
     if (want & 1u) oracle_replica_mean(x, 0, K, P);
     for (int j = 0; j < N; ++j)
       if (want & (1u << (j + 1))) oracle_replica_mean(u[j], 0, K, P);
@@ -196,8 +209,40 @@ static int run_case(const drv_case* t) {
     CHECK_HIP(hipStreamSynchronize(st)); /* g is rewritten next step */
   }
 
-  /* every state of every worker, read back through the ABI */
+  /* every state averaged with its diagnostics */
   const int nstates = 1 + N + (has_v ? 1 : 0);
+  double stats_worst = 0.0;
+  if (t->stats) {
+    size_t sb = 0;
+    CHECK_MT(NULL, mtdao_stats_scratch_bytes(&c, &sb));
+    void* scratch = NULL;
+    CHECK_HIP(hipMalloc(&scratch, sb));
+    double hs[(MTDAO_MAX_N + 2) * MTDAO_STATS_STRIDE];
+    const uint32_t full = (1u << nstates) - 1u;
+    uint32_t applied = 0;
+    CHECK_MT(h, mtdao_sync_stats(h, full, &applied, scratch, sb, hs, (void*)st));
+    if (applied != full) masks_ok = 0;
+    double* want = malloc((size_t)(4 + 2 * K) * sizeof(double));
+    for (int sid = 0; sid < nstates; ++sid) {
+      float* ref = sid == 0 ? x : (sid <= N ? u[sid - 1] : v);
+      oracle_state_stats(ref, 0, NULL, K, P, want);
+      oracle_replica_mean(ref, 0, K, P);
+      const double* got = hs + (size_t)sid * MTDAO_STATS_STRIDE;
+      double big = 0.0;
+      for (int k = 0; k < 4 + 2 * K; ++k) big = fmax(big, fabs(want[k]));
+      for (int k = 0; k < 3 + 2 * K; ++k) {
+        const int wi = k < 3 ? k : k + 1; /* oracle: [mean_sq, var, outer_sq, 0, sq[K], dot[K]] */
+        const int gi = k < 3 ? k : (k < 3 + K ? MTDAO_STAT_WORKER_SQ + (k - 3) : MTDAO_STAT_WORKER_DOT + (k - 3 - K));
+        const double den = fmax(fabs(want[wi]), 1e-6 * big);
+        const double e = den > 0.0 ? fabs(got[gi] - want[wi]) / den : fabs(got[gi] - want[wi]);
+        if (!(e <= stats_worst)) stats_worst = e;
+      }
+    }
+    free(want);
+    CHECK_HIP(hipFree(scratch));
+  }
+
+  /* every state of every worker, read back through the ABI */
   double worst = 0.0;
   for (int sid = 0; sid < nstates; ++sid) {
     const float* ref = sid == 0 ? x : (sid <= N ? u[sid - 1] : v);
@@ -208,9 +253,11 @@ static int run_case(const drv_case* t) {
   }
   const int64_t count = mtdao_step_count(h);
   mtdao_destroy(h);
-  const int ok = masks_ok && worst <= 1e-5 && count == t->steps;
-  printf("%s: K=%d P=%lld N=%d steps=%d state-syncs=%u max rel err %.3e masks %s -> %s\n", t->name, K,
-         (long long)P, N, t->steps, nsync, worst, masks_ok ? "match" : "DIFFER", ok ? "ok" : "FAIL");
+  const int ok = masks_ok && worst <= 1e-5 && stats_worst <= 1e-5 && count == t->steps;
+  printf("%s: K=%d P=%lld N=%d steps=%d state-syncs=%u max rel err %.3e", t->name, K, (long long)P, N, t->steps,
+         nsync, worst);
+  if (t->stats) printf(" diagnostics err %.3e", stats_worst);
+  printf(" masks %s -> %s\n", masks_ok ? "match" : "DIFFER", ok ? "ok" : "FAIL");
   fflush(stdout);
 
   CHECK_HIP(hipFree(dx));
@@ -228,13 +275,15 @@ static int run_case(const drv_case* t) {
 }
 
 int main(void) {
-  const drv_case cases[2] = {
+  const drv_case cases[3] = {
       {"adam_n3_k4_step_sync", MTDAO_ADAM, 4, 3, 10007, {0.9f, 0.99f, 0.999f}, {0.3f, 0.3f, 0.3f}, 0.999f, 1e-8f,
-       0.0f, 1e-3f, 4, {8, 8, 16}, 16, 32, 1},
+       0.0f, 1e-3f, 4, {8, 8, 16}, 16, 32, 1, 0},
       {"sgdm_n2_k5_clip_sync", MTDAO_SGDM, 5, 2, 8204, {0.9f, 0.99f}, {0.3f, 0.6f}, 0.0f, 0.0f, 0.05f, 1e-2f, 4,
-       {2, 8}, 0, 24, 0},
+       {2, 8}, 0, 24, 0, 0},
+      {"adam_n2_k6_sync_stats", MTDAO_ADAM, 6, 2, 4099, {0.9f, 0.99f}, {0.4f, 0.4f}, 0.999f, 1e-8f, 0.0f, 1e-3f, 4,
+       {0, 0}, 0, 6, 0, 1},
   };
   int all = 1;
-  for (int i = 0; i < 2; ++i) all &= run_case(&cases[i]);
+  for (int i = 0; i < 3; ++i) all &= run_case(&cases[i]);
   return all ? 0 : 1;
 }

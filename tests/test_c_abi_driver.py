@@ -2,10 +2,12 @@
 
 The driver allocates with hipMalloc, enqueues on a HIP stream of its own
 and has no Python or torch on its path.  It runs an Adam case through
-mtdao_step_sync and a clipped SGDM case through mtdao_local_step +
-mtdao_sync.  Every state it reads back through mtdao_read_state is checked
-against the CPU oracle on the same inputs, and every applied mask against
-the oracle's schedule.
+mtdao_step_sync, a clipped SGDM case through mtdao_local_step +
+mtdao_sync, and an Adam case that ends with mtdao_sync_stats of every
+state.  Every state it reads back through mtdao_read_state is checked
+against the CPU oracle on the same inputs, the diagnostics against the
+oracle's, and every applied mask and mtdao_schedule against the oracle's
+schedule.
 """
 
 import os
@@ -39,9 +41,9 @@ def test_driver_links_the_in_tree_libraries():
 
 @pytest.mark.gpu
 def test_c_driver_matches_oracle():
-    print("c-abi driver: adam_n3_k4_step_sync, sgdm_n2_k5_clip_sync", flush=True)
+    print("c-abi driver: adam_n3_k4_step_sync, sgdm_n2_k5_clip_sync, adam_n2_k6_sync_stats", flush=True)
     r = subprocess.run([BIN], capture_output=True, text=True, timeout=180)
     print(r.stdout, r.stderr, flush=True)
     assert r.returncode == 0, r.stderr
     lines = [ln for ln in r.stdout.splitlines() if ln.strip()]
-    assert len(lines) == 2 and all(ln.endswith("-> ok") for ln in lines), r.stdout
+    assert len(lines) == 3 and all(ln.endswith("-> ok") for ln in lines), r.stdout
