@@ -857,3 +857,42 @@ def test_random_sync_stats(seed):
     a.close()
     b.close()
     torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("name,k,fused", [("adam_n3_k4_p16m", 5, False), ("adam_n3_k4_p16m", -3, True),
+                                          ("adopt_n2_k8_p124m_bf16", 4, False), ("adopt_n2_k8_p124m_bf16", -2, True)],
+                         ids=["adam_up", "adam_down_fused", "adopt_bf16_up", "adopt_bf16_down_fused"])
+def test_power_of_two_gradient_scale_invariance(name, k, fused):
+    """With eps = 0, scaling every gradient by 2^k leaves the Adam and ADOPT
+    trajectories of x unchanged bit for bit on the GPU (averaging events
+    included): v scales by 4^k, Adam's u by 2^k, ADOPT's u not at all,
+    because a power-of-two scale commutes with every fp32 rounding, the
+    square root and the division.  No oracle is involved."""
+    w = synth.small_variant(synth.WORKLOADS[name], 30_000, tail=8)
+    w = w.replace(eps=0.0, steps=24, period_x=4, period_u=(6,) * w.n_moments, period_v=8)
+    log(f"case scale {w.name} k={k} fused={fused}")
+    d = torch.device("cuda:0")
+    dev = DeviceInputs(w, d)
+    gdt = torch.bfloat16 if w.grad_dtype == "bf16" else torch.float32
+    grads = torch.empty((w.replicas, w.numel), dtype=gdt, device=d)
+    opts = []
+    for scale in (1.0, 2.0 ** k):
+        opt = MtdaoOptimizer(abi.config_from_workload(w), d, x0=dev.x0_row())
+        for s in _steps(w):
+            dev.grads_into(s, grads)
+            grads.mul_(scale)
+            if fused:
+                opt.step_sync(grads, w.lr, w.adopt_clip_value(s))
+            else:
+                opt.step(grads, w.lr, w.adopt_clip_value(s))
+                opt.sync()
+        opts.append(opt)
+    torch.cuda.synchronize()
+    a, b = opts
+    assert torch.equal(a.x, b.x)
+    u_scale = 2.0 ** k if w.form == "adam" else 1.0
+    for ua, ub in zip(a.u, b.u):
+        assert torch.equal(ua * u_scale, ub)
+    assert torch.equal(a.v * 4.0 ** k, b.v)
+    a.close()
+    b.close()
