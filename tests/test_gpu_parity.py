@@ -896,3 +896,57 @@ def test_power_of_two_gradient_scale_invariance(name, k, fused):
     assert torch.equal(a.v * 4.0 ** k, b.v)
     a.close()
     b.close()
+
+
+@pytest.mark.parametrize("name", ["adam_n3_k4_p16m", "adopt_n2_k8_p124m_bf16", "sgdm_n2_k16_p354m_clip"])
+def test_identical_workers_equal_one_worker(name):
+    """K workers that all receive worker 0's gradient follow, bit for bit,
+    the trajectory of a single worker: averaging identical rows is an exact
+    no-op, the clip norms agree, and the K = 1 launch shapes (half-row
+    windows, no averaging) compute the same per-element arithmetic as the
+    replica-pair windows and the averaging kernels.  No oracle is involved."""
+    w = synth.small_variant(synth.WORKLOADS[name], 30_000, tail=37)
+    w = w.replace(replicas=6, steps=20, period_x=3, period_u=(4,) * w.n_moments, period_v=5)
+    log(f"case identical workers {w.name}")
+    d = torch.device("cuda:0")
+    dev = DeviceInputs(w, d)
+    gdt = torch.bfloat16 if w.grad_dtype == "bf16" else torch.float32
+    grads = torch.empty((w.replicas, w.numel), dtype=gdt, device=d)
+    many = MtdaoOptimizer(abi.config_from_workload(w), d, x0=dev.x0_row())
+    one = MtdaoOptimizer(abi.config_from_workload(w.replace(replicas=1)), d, x0=dev.x0_row())
+    for s in _steps(w):
+        dev.grads_into(s, grads)
+        grads[1:] = grads[0:1]
+        many.step_sync(grads, w.lr, w.adopt_clip_value(s))
+        one.step(grads[0:1].contiguous(), w.lr, w.adopt_clip_value(s))
+        one.sync()
+    torch.cuda.synchronize()
+    for a, b in zip(many.states(), one.states()):
+        assert torch.equal(a, b.expand_as(a))
+    many.close()
+    one.close()
+
+
+@pytest.mark.parametrize("name", ["adam_n3_k4_p16m", "sgdm_n2_k16_p354m_clip"])
+def test_worker_permutation_permutes_states(name):
+    """Without averaging, permuting the workers' gradients permutes every
+    state bit for bit (each worker's update depends on its own row and its
+    own clip norm only).  No oracle is involved."""
+    w = synth.small_variant(synth.WORKLOADS[name], 30_000, tail=8)
+    w = w.replace(replicas=5, steps=12, period_x=0, period_u=(0,) * w.n_moments, period_v=0)
+    log(f"case permutation {w.name}")
+    d = torch.device("cuda:0")
+    dev = DeviceInputs(w, d)
+    perm = torch.tensor([3, 0, 4, 1, 2], device=d)
+    grads = torch.empty((w.replicas, w.numel), dtype=torch.float32, device=d)
+    a = MtdaoOptimizer(abi.config_from_workload(w), d, x0=dev.x0_row())
+    b = MtdaoOptimizer(abi.config_from_workload(w), d, x0=dev.x0_row())
+    for s in _steps(w):
+        dev.grads_into(s, grads)
+        a.step(grads, w.lr)
+        b.step(grads[perm].contiguous(), w.lr)
+    torch.cuda.synchronize()
+    for p, q in zip(a.states(), b.states()):
+        assert torch.equal(p[perm], q)
+    a.close()
+    b.close()
