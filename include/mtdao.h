@@ -94,7 +94,13 @@ enum { MTDAO_SYNC_AFTER_STEP = 0, MTDAO_SYNC_MOMENTA_IN_STEP = 1 };
  *                         d = xo - E_m[x^m]; b = mu b + d;
  *                         xo = xo - outer_lr (d + mu b); every worker
  *                         restarts from xo.  outer_lr = 1, mu = 0 is
- *                         averaging.  Needs sync_order AFTER_STEP. */
+ *                         averaging.  Needs sync_order AFTER_STEP.  The
+ *                         outer step runs at most once per step s: a
+ *                         later averaging of x at the same s (mtdao_sync
+ *                         after mtdao_step_sync, a repeated mtdao_sync,
+ *                         mtdao_sync_stats after mtdao_sync) only averages
+ *                         rows that are already equal, so it changes
+ *                         nothing. */
 enum { MTDAO_OUTER_AVERAGE = 0, MTDAO_OUTER_NESTEROV = 1 };
 /* State ids of mtdao_read_state beyond the per-worker states
  * (0 = x, 1..N = u^j, N+1 = v): the outer parameters and momentum of the
@@ -212,7 +218,8 @@ int32_t mtdao_local_step(mtdao_handle* h, const void* grads, float lr, float ado
  * every selected state becomes S^0 + (sum_{m>=1} (S^m - S^0)) / K, the
  * differences summed in fp64 and the result rounded once to the storage
  * type, and is written to all K rows, so averaging identical rows is an
- * exact no-op and a repeated call at the same s changes nothing.
+ * exact no-op and a repeated call at the same s changes nothing (also under
+ * the Nesterov OuterOpt, whose outer step runs once per s).
  * applied_mask (may be NULL) receives the set actually averaged. */
 int32_t mtdao_sync(mtdao_handle* h, uint32_t mask, uint32_t* applied_mask, void* hip_stream);
 

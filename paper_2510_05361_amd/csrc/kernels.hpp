@@ -174,8 +174,9 @@ __host__ __device__ constexpr int64_t tiles_for(int64_t P) {
 struct OuterParams {
   float* xo;
   float* mom;
-  float lr;   // outer learning rate
-  float mu;   // outer momentum
+  float lr;        // outer learning rate
+  float mu;        // outer momentum
+  int32_t update;  // 0: xo and mom are only read (the outer step of this s already ran)
 };
 
 // xbar (the workers' mean) becomes the value every worker restarts from:
@@ -183,7 +184,7 @@ struct OuterParams {
 template <int V>
 __device__ __forceinline__ void outer_step(const OuterParams& o, int64_t e, float (&xbar)[V]) {
 #pragma clang fp contract(off)
-  if (o.xo == nullptr) return;
+  if (o.xo == nullptr || !o.update) return;
   float xo[V], b[V];
   load_v<float, V, false>(o.xo, e, xo);
   load_v<float, V, false>(o.mom, e, b);

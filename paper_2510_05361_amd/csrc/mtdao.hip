@@ -30,6 +30,7 @@ struct mtdao_handle {
   double* partials = nullptr;       // workspace: [K][norm_blocks]
   int32_t norm_blocks = 0;
   int64_t s = 0;                    // local updates applied
+  int64_t outer_done_s = -1;        // Nesterov: step s whose outer step has run
   std::string err;
 };
 
@@ -593,13 +594,25 @@ int32_t resolve_mask(mtdao_handle* h, uint32_t mask, int64_t s, uint32_t* out) {
   return MTDAO_OK;
 }
 
-OuterParams outer_params(const mtdao_handle* h) {
+OuterParams outer_params(const mtdao_handle* h, bool update = true) {
   OuterParams o;
   o.xo = h->x_outer;
   o.mom = h->x_outer_mom;
   o.lr = h->cfg.outer_lr;
   o.mu = h->cfg.outer_momentum;
+  o.update = update ? 1 : 0;
   return o;
+}
+
+// The Nesterov outer step runs at most once per step s: an averaging of x
+// that repeats the one of this s (mtdao_sync after mtdao_step_sync, a second
+// mtdao_sync or mtdao_sync_stats) only averages rows that are already equal.
+// Returns whether the outer step is to run now and records it.
+bool claim_outer_step(mtdao_handle* h, uint32_t work, int64_t s) {
+  if (!h->x_outer || !(work & 1u)) return false;
+  if (h->outer_done_s == s) return false;
+  h->outer_done_s = s;
+  return true;
 }
 
 // Per-step scalars of update s in double, rounded once to fp32; launches
@@ -659,7 +672,7 @@ void launch_adopt_first(mtdao_handle* h, const void* grads, hipStream_t st) {
   else launch_adopt_init<uint16_t>(grads, h->v, c.numel, c.replicas, Vi, st);
 }
 
-void launch_means(mtdao_handle* h, uint32_t m, hipStream_t st) {
+void launch_means(mtdao_handle* h, uint32_t m, bool outer_update, hipStream_t st) {
   const mtdao_config& c = h->cfg;
   MeanParams mp;
   std::memset(&mp, 0, sizeof mp);
@@ -670,7 +683,7 @@ void launch_means(mtdao_handle* h, uint32_t m, hipStream_t st) {
   // fp32 moment states (and fp32 x) in one launch, bf16 x in its own
   int n = 0;
   if ((m & 1u) && c.param_dtype == MTDAO_F32) {
-    if (h->x_outer) mp.outer_state = n;
+    if (outer_update) mp.outer_state = n;
     mp.state[n++] = h->x;
   }
   for (int j = 0; j < c.n_moments; ++j)
@@ -680,7 +693,7 @@ void launch_means(mtdao_handle* h, uint32_t m, hipStream_t st) {
   if ((m & 1u) && c.param_dtype == MTDAO_BF16) {
     MeanParams xp = mp;
     xp.state[0] = h->x;
-    xp.outer_state = h->x_outer ? 0 : -1;
+    xp.outer_state = outer_update ? 0 : -1;
     launch_mean<uint16_t>(xp, 1, vec_width(MTDAO_BF16, c.numel), st);
   }
 }
@@ -712,25 +725,36 @@ int32_t mtdao_sync(mtdao_handle* h, uint32_t mask, uint32_t* applied_mask, void*
     return fail(&h->err, MTDAO_ERR_INVALID_ARG,
                 "with sync_order MOMENTA_IN_STEP the moments are averaged inside mtdao_step_sync (mask 0x%x)", m);
   if (applied_mask) *applied_mask = m;
+  if (c.numel == 0) return MTDAO_OK;
+  const bool outer_update = claim_outer_step(h, m, h->s);
   // K = 1: the mean is the row; only an outer step on x still has work
-  const uint32_t work = c.replicas > 1 ? m : (h->x_outer ? (m & 1u) : 0u);
-  if (work == 0 || c.numel == 0) return MTDAO_OK;
-  launch_means(h, work, reinterpret_cast<hipStream_t>(hip_stream));
+  const uint32_t work = c.replicas > 1 ? m : (outer_update ? 1u : 0u);
+  if (work == 0) return MTDAO_OK;
+  launch_means(h, work, outer_update, reinterpret_cast<hipStream_t>(hip_stream));
   return hip_check(&h->err, hipGetLastError(), "mtdao_sync launch");
 }
 
-int32_t mtdao_sync_stats(mtdao_handle* h, uint32_t mask, uint32_t* applied_mask, void* scratch, size_t scratch_bytes,
-                         double* host_stats, void* hip_stream) {
-  if (!h) return fail(&g_err, MTDAO_ERR_INVALID_ARG, "handle is NULL");
+}  // extern "C"
+
+namespace {
+
+// Checks shared by both diagnostics entry points (before any scratch check).
+int32_t check_stats_args(mtdao_handle* h, double* host_stats) {
   const mtdao_config& c = h->cfg;
   if (c.replicas > kStatsMaxK)
     return fail(&h->err, MTDAO_ERR_INVALID_ARG, "diagnostics support up to %d replicas (K=%d)", kStatsMaxK, c.replicas);
   if (!host_stats) return fail(&h->err, MTDAO_ERR_INVALID_ARG, "host_stats is NULL");
-  const size_t need = stats_scratch_for(c);
-  if (!scratch || scratch_bytes < need)
-    return fail(&h->err, MTDAO_ERR_WORKSPACE, "stats scratch of %zu bytes required", need);
-  if ((reinterpret_cast<uintptr_t>(scratch) & 255u) != 0)
-    return fail(&h->err, MTDAO_ERR_ALIGN, "stats scratch is not 256-byte aligned");
+  return MTDAO_OK;
+}
+
+// mtdao_sync_stats after its scratch checks: the averaging with the
+// diagnostics of every averaged state, partial sums in `scratch` (at least
+// stats_scratch_for(cfg) bytes, 256-byte aligned; every word the kernels
+// read is written first in the same call, so nothing needs clearing), the
+// finalized rows copied to host_stats through a buffer on the stack.
+int32_t run_sync_stats(mtdao_handle* h, uint32_t mask, uint32_t* applied_mask, double* scratch, double* host_stats,
+                       hipStream_t st) {
+  const mtdao_config& c = h->cfg;
   uint32_t m;
   int32_t r = resolve_mask(h, mask, h->s, &m);
   if (r != MTDAO_OK) return r;
@@ -738,11 +762,10 @@ int32_t mtdao_sync_stats(mtdao_handle* h, uint32_t mask, uint32_t* applied_mask,
     return fail(&h->err, MTDAO_ERR_INVALID_ARG,
                 "with sync_order MOMENTA_IN_STEP the moments are averaged inside mtdao_step_sync (mask 0x%x)", m);
   if (applied_mask) *applied_mask = m;
-  const int nslots = 2 + kMaxN;
+  constexpr int nslots = 2 + kMaxN;
   for (int i = 0; i < nslots * kStatsStride; ++i) host_stats[i] = NAN;
   if (m == 0 || c.numel == 0) return MTDAO_OK;
-  hipStream_t st = reinterpret_cast<hipStream_t>(hip_stream);
-  double* partials = reinterpret_cast<double*>(scratch);
+  double* partials = scratch;
   size_t fp32_part, bf16_part;
   stats_scratch_doubles(c, &fp32_part, &bf16_part);
   double* part_x = partials + fp32_part;
@@ -754,7 +777,9 @@ int32_t mtdao_sync_stats(mtdao_handle* h, uint32_t mask, uint32_t* applied_mask,
   mp.P = c.numel;
   mp.K = c.replicas;
   mp.outer_state = -1;
-  mp.outer = outer_params(h);
+  // under Nesterov the diagnostics of x are those of the pseudo-gradients
+  // x_outer - x^m also when the outer step of this s has already run
+  mp.outer = outer_params(h, claim_outer_step(h, m, h->s));
   int n = 0;
   if ((m & 1u) && c.param_dtype == MTDAO_F32) {
     if (h->x_outer) mp.outer_state = n;
@@ -781,17 +806,34 @@ int32_t mtdao_sync_stats(mtdao_handle* h, uint32_t mask, uint32_t* applied_mask,
   }
   r = hip_check(&h->err, hipGetLastError(), "mtdao_sync_stats launch");
   if (r != MTDAO_OK) return r;
-  std::vector<double> rows((size_t)2 * nslots * kStatsStride);
-  r = hip_check(&h->err, hipMemcpyAsync(rows.data(), out, rows.size() * sizeof(double), hipMemcpyDeviceToHost, st),
-                "mtdao_sync_stats copy");
+  double rows[2 * nslots * kStatsStride];
+  r = hip_check(&h->err, hipMemcpyAsync(rows, out, sizeof rows, hipMemcpyDeviceToHost, st), "mtdao_sync_stats copy");
   if (r != MTDAO_OK) return r;
   r = hip_check(&h->err, hipStreamSynchronize(st), "mtdao_sync_stats wait");
   if (r != MTDAO_OK) return r;
   for (int i = 0; i < n; ++i)
-    for (int k = 0; k < kStatsStride; ++k) host_stats[ids[i] * kStatsStride + k] = rows[(size_t)i * kStatsStride + k];
+    for (int k = 0; k < kStatsStride; ++k) host_stats[ids[i] * kStatsStride + k] = rows[i * kStatsStride + k];
   if (bf16_x)
-    for (int k = 0; k < kStatsStride; ++k) host_stats[k] = rows[(size_t)nslots * kStatsStride + k];
+    for (int k = 0; k < kStatsStride; ++k) host_stats[k] = rows[nslots * kStatsStride + k];
   return MTDAO_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t mtdao_sync_stats(mtdao_handle* h, uint32_t mask, uint32_t* applied_mask, void* scratch, size_t scratch_bytes,
+                         double* host_stats, void* hip_stream) {
+  if (!h) return fail(&g_err, MTDAO_ERR_INVALID_ARG, "handle is NULL");
+  int32_t r = check_stats_args(h, host_stats);
+  if (r != MTDAO_OK) return r;
+  const size_t need = stats_scratch_for(h->cfg);
+  if (!scratch || scratch_bytes < need)
+    return fail(&h->err, MTDAO_ERR_WORKSPACE, "stats scratch of %zu bytes required", need);
+  if ((reinterpret_cast<uintptr_t>(scratch) & 255u) != 0)
+    return fail(&h->err, MTDAO_ERR_ALIGN, "stats scratch is not 256-byte aligned");
+  return run_sync_stats(h, mask, applied_mask, reinterpret_cast<double*>(scratch), host_stats,
+                        reinterpret_cast<hipStream_t>(hip_stream));
 }
 
 int32_t mtdao_step_sync(mtdao_handle* h, const void* grads, float lr, float adopt_clip, uint32_t mask,
@@ -809,11 +851,13 @@ int32_t mtdao_step_sync(mtdao_handle* h, const void* grads, float lr, float adop
   if (c.numel == 0) return MTDAO_OK;
   hipStream_t st = reinterpret_cast<hipStream_t>(hip_stream);
   const StepParams p = prepare_step(h, grads, lr, adopt_clip, s, st);
+  // s is new, so an outer step due here has not run yet
+  const bool outer_update = claim_outer_step(h, m, s);
   // K = 1: the mean is the row; only an outer step on x still has work
-  const uint32_t work = c.replicas > 1 ? m : (h->x_outer ? (m & 1u) : 0u);
+  const uint32_t work = c.replicas > 1 ? m : (outer_update ? 1u : 0u);
   if (adopt_first_update(c, s)) {
     launch_adopt_first(h, grads, st);
-    if (work != 0) launch_means(h, work, st);
+    if (work != 0) launch_means(h, work, outer_update, st);
   } else if (work == 0) {
     launch_step(c, p, step_vec_width(c), st);
   } else if (c.sync_order == MTDAO_SYNC_MOMENTA_IN_STEP && (work & ~1u) != 0) {

@@ -14,7 +14,8 @@ import torch
 
 import oracle
 import synth
-from gpu_harness import compare, free, gather_state, log, run_gpu, run_oracle
+from gpu_harness import (OracleResult, XAbsMax, compare, free, gather_state, log, run_gpu, run_oracle,
+                         run_oracle_parallel)
 from paper_2510_05361_amd import mtdao as abi
 from paper_2510_05361_amd.optimizer import MtdaoOptimizer
 from synth.device import DeviceInputs
@@ -55,22 +56,95 @@ def test_small_variant_full_compare(name, tail):
     free(g)
 
 
+FULL_EVERY_ELEMENT = ("adam_n2_k2_p1m", "adam_n3_k4_p16m", "adopt_n2_k8_p124m_bf16")
+
+
+@pytest.mark.timeout(900)
 @pytest.mark.parametrize("name", NAMES)
-def test_full_size_sampled(name):
-    """Every workload at its full size for all its steps.  Workloads whose
-    oracle run stays under 10^8 element-updates are compared on every
-    element; the others on a deterministic sample (each element's
-    trajectory depends only on its own inputs)."""
+def test_full_size(name):
+    """Every workload at its full size for all its steps, through
+    mtdao_step_sync (the call and launch configuration the benchmark
+    times).  The 1M, 16.8M and 124M-parameter workloads are compared on
+    every element of every replica, and their separate calls
+    (mtdao_local_step + mtdao_sync) must give the same states bit for bit;
+    the 1.31B and 354M ones on a sample of more than 2^20 elements per
+    replica: 2^20 strided columns (the unbiased subset the rms floor is
+    taken over), the first and last 64 elements of every tensor and the
+    columns around the flat-index and byte-offset boundaries 2^29..2^33."""
     w = synth.WORKLOADS[name]
-    idx = None if w.numel * w.replicas * w.steps <= 10 ** 8 else synth.sample_indices(w)
+    every = name in FULL_EVERY_ELEMENT
+    idx = None if every else synth.sample_indices(w)
     log(f"case full {w.name} P={w.numel} K={w.replicas} T={w.steps} "
-        f"compared={'all' if idx is None else idx.size}")
-    g = run_gpu(w, _steps(w))
+        f"compared={'all' if idx is None else idx.size} columns")
+    g = run_gpu(w, _steps(w), fused=True)
     log("  gpu done")
-    o = run_oracle(w, _steps(w), idx)
+    if every:
+        sep = run_gpu(w, _steps(w))
+        assert sep.masks == g.masks
+        for p, q in zip(sep.opt.states(), g.opt.states()):
+            assert torch.equal(p, q)
+        free(sep)
+    o = run_oracle_parallel(w, _steps(w), idx, rms_cols=None if every else synth.strided_mask(w, idx))
     assert g.masks == o.masks
-    compare(w, g.opt, o, w.name)
+    compare(w, g.opt, o, f"full-{w.name}")
     free(g)
+
+
+@pytest.mark.parametrize("name", ["adam_n3_k4_p1311m", "sgdm_n2_k16_p354m_clip"])
+def test_full_size_every_element_written(name):
+    """Write coverage of the full-size launches, on every element of every
+    replica: SGDM with N = 1, beta = 0, omega = 1, lr = 1 and no clip makes
+    one update u = g and x = x0 - g exactly (one fp32 rounding, as torch's
+    subtraction), so the plain step (tile placement, replica-pair windows)
+    must leave exactly those values; then the standalone mean of x and u
+    and a fused step with x and u due must leave every row equal to
+    S^0 + (sum_{m>=1} (S^m - S^0)) / K formed in fp64 in replica order and
+    rounded once (K = 4 and 16 make 1/K exact), computed here with torch."""
+    base = synth.WORKLOADS[name]
+    w = base.replace(form="sgdm", beta1=(0.0,), omega=(1.0,), lr=1.0, clip_rho=0.0, period_x=0, period_u=(0,),
+                     period_v=0, steps=2)
+    K, P = w.replicas, w.numel
+    log(f"case coverage {name} P={P} K={K}")
+    d = torch.device("cuda:0")
+    dev = DeviceInputs(w, d)
+    opt = MtdaoOptimizer(abi.config_from_workload(w), d, x0=dev.x0_row())
+    grads = torch.empty((K, P), dtype=torch.float32, device=d)
+    x0 = dev.x0_row()
+    dev.grads_into(1, grads)
+    opt.step(grads, 1.0)
+    torch.cuda.synchronize()
+    for m in range(K):
+        assert torch.equal(opt.x[m], x0 - grads[m]), m
+        assert torch.equal(opt.u[0][m], grads[m]), m
+
+    def assert_rows_are_mean(t, rows, what):
+        # rows(m, lo, hi) -> the pre-average fp32 values of row m, columns [lo, hi)
+        step = 1 << 28
+        for lo in range(0, P, step):
+            hi = min(P, lo + step)
+            s0 = rows(0, lo, hi).double()
+            acc = torch.zeros_like(s0)
+            for m in range(1, K):
+                acc += rows(m, lo, hi).double() - s0
+            want = (s0 + acc * (1.0 / K)).float()
+            for m in range(K):
+                assert torch.equal(t[m, lo:hi], want), (what, m, lo)
+
+    before_x, before_u = opt.x.clone(), opt.u[0].clone()
+    assert opt.sync(0b11) == 0b11
+    torch.cuda.synchronize()
+    assert_rows_are_mean(opt.x, lambda m, lo, hi: before_x[m, lo:hi], "mean x")
+    assert_rows_are_mean(opt.u[0], lambda m, lo, hi: before_u[m, lo:hi], "mean u")
+    del before_x, before_u
+    xbar = opt.x[0].clone()
+    dev.grads_into(2, grads)
+    assert opt.step_sync(grads, 1.0, 0.0, 0b11) == 0b11
+    torch.cuda.synchronize()
+    assert_rows_are_mean(opt.x, lambda m, lo, hi: xbar[lo:hi] - grads[m, lo:hi], "fused x")
+    assert_rows_are_mean(opt.u[0], lambda m, lo, hi: grads[m, lo:hi], "fused u")
+    opt.close()
+    del opt, grads, x0, xbar
+    torch.cuda.empty_cache()
 
 
 EDGE = {
@@ -153,6 +227,7 @@ def test_zero_gradient_replica_and_zero_gradients():
     opt = MtdaoOptimizer(cfg, d, x0=dev.x0_row())
     ocfg = oracle.OracleConfig.from_workload(w)
     ost = oracle.new_state(ocfg, synth.host_x0_row(w), w.replicas)
+    track = XAbsMax(ost)
     grads = torch.empty((w.replicas, w.numel), dtype=torch.float32, device=d)
     for s in range(1, w.steps + 1):
         dev.grads_into(s, grads)
@@ -168,10 +243,10 @@ def test_zero_gradient_replica_and_zero_gradients():
         opt.step(grads, w.lr)
         m = opt.sync()
         oracle.run(ocfg, ost, lambda s_: hg2, [s], lambda s_: w.lr)
+        track.update(ost)
         assert m == oracle.schedule(ocfg, s)
     torch.cuda.synchronize()
-    from gpu_harness import OracleResult
-    compare(w, opt, OracleResult(ost, [], None), "zero-grad")
+    compare(w, opt, OracleResult(ost, [], None, x_absmax=[track.a], steps=w.steps), "zero-grad")
     opt.close()
 
 
@@ -378,11 +453,14 @@ def test_step_sync_explicit_masks_and_first_step(form):
         assert torch.equal(p, q)
     ocfg = oracle.OracleConfig.from_workload(w)
     ost = oracle.new_state(ocfg, synth.host_x0_row(w), w.replicas)
-    from gpu_harness import OracleResult, oracle_clip_scales
-    oracle.run(ocfg, ost, lambda s: synth.host_grad_rows(w, s), _steps(w), lambda s: w.lr,
-               w.adopt_clip_value, scales=lambda s, g: oracle_clip_scales(w, s),
-               masks=lambda s: masks[s - 1])
-    compare(w, fused, OracleResult(ost, masks, None), f"explicit-{form}")
+    track = XAbsMax(ost)
+    from gpu_harness import oracle_clip_scales
+    for s in _steps(w):
+        oracle.run(ocfg, ost, lambda s_: synth.host_grad_rows(w, s_), [s], lambda s_: w.lr,
+                   w.adopt_clip_value, scales=lambda s_, g: oracle_clip_scales(w, s_),
+                   masks=lambda s_: masks[s_ - 1])
+        track.update(ost)
+    compare(w, fused, OracleResult(ost, masks, None, x_absmax=[track.a]), f"explicit-{form}")
     fused.close()
     free(sep)
 
@@ -412,15 +490,13 @@ def test_step_sync_full_size_bench_workload():
         applied.append(opt.step_sync(grads, w.lr))
     torch.cuda.synchronize()
     idx = synth.sample_indices(w)
-    ocfg = oracle.OracleConfig.from_workload(w)
-    ost = oracle.OracleState(synth.host_pool_rows(w, 11, 0.02, idx),
-                             [synth.host_pool_rows(w, 12 + j, 1e-3, idx) for j in range(3)],
-                             synth.host_pool_rows(w, 15, 1e-6, idx, absolute=True))
-    masks = oracle.run(ocfg, ost, lambda s: synth.host_grad_rows(w, s, idx), range(start + 1, w.steps + 1),
-                       lambda s: w.lr)
-    assert applied == masks == [0] * 7 + [0b11111]
-    from gpu_harness import OracleResult
-    compare(w, opt, OracleResult(ost, masks, idx), "fused-full")
+    o = run_oracle_parallel(
+        w, range(start + 1, w.steps + 1), idx, rms_cols=synth.strided_mask(w, idx),
+        init=lambda c: oracle.OracleState(synth.host_pool_rows(w, 11, 0.02, c),
+                                          [synth.host_pool_rows(w, 12 + j, 1e-3, c) for j in range(3)],
+                                          synth.host_pool_rows(w, 15, 1e-6, c, absolute=True)))
+    assert applied == o.masks == [0] * 7 + [0b11111]
+    compare(w, opt, o, "fused-full")
     opt.close()
     del x, u, v, grads
     torch.cuda.empty_cache()
@@ -468,10 +544,13 @@ def test_probabilistic_sync_against_oracle(size):
     idx = synth.sample_indices(w) if size == "full" else None
     ocfg = oracle.OracleConfig.from_workload(w)
     ost = oracle.new_state(ocfg, synth.host_x0_row(w, idx), w.replicas)
-    oracle.run_probabilistic(ocfg, ost, lambda s: synth.host_grad_rows(w, s, idx), _steps(w),
-                             lambda s: w.lr, lambda s: masks[s - 1])
-    from gpu_harness import OracleResult
-    compare(w, opt, OracleResult(ost, masks, idx), f"prob-{size}")
+    track = XAbsMax(ost)
+    for s in _steps(w):
+        oracle.run_probabilistic(ocfg, ost, lambda s_: synth.host_grad_rows(w, s_, idx), [s],
+                                 lambda s_: w.lr, lambda s_: masks[s_ - 1])
+        track.update(ost)
+    compare(w, opt, OracleResult(ost, masks, idx, rms_cols=None if idx is None else synth.strided_mask(w, idx),
+                                 x_absmax=[track.a]), f"prob-{size}")
     opt.close()
     torch.cuda.empty_cache()
 
@@ -546,6 +625,36 @@ def test_outer_nesterov_fused_bit_identical_and_resume():
     free(a, b, c, r)
 
 
+@pytest.mark.parametrize("name,K", [("adam_n3_k4_p16m", 4), ("adopt_n2_k8_p124m_bf16", 8), ("adam_n3_k4_p16m", 1)],
+                         ids=["fp32_k4", "bf16x_k8", "fp32_k1"])
+@pytest.mark.parametrize("fused", [False, True], ids=["separate", "fused"])
+def test_outer_nesterov_repeated_averaging_changes_nothing(name, K, fused):
+    """Under the Nesterov OuterOpt the outer step runs once per step s: after
+    the averaging of x at s (fused or separate), a second mtdao_sync, a
+    mtdao_sync_stats and a third mtdao_sync at the same s leave x, the outer
+    parameters and the outer momentum bit for bit as they were, and the
+    states still equal the oracle's (which takes one outer step per event).
+    The repeated diagnostics of x are those of pseudo-gradients that are
+    all zero (fp32) or the rounding residual x_outer - bf16(x_outer)."""
+    w = synth.small_variant(synth.WORKLOADS[name], 20_000, tail=8).replace(replicas=K, steps=8, period_x=4)
+    log(f"case nesterov repeat {w.name} K={K} fused={fused}")
+    g = run_gpu(w, _steps(w), outer=NESTEROV, fused=fused)
+    assert g.masks[-1] & 1
+    keep = [t.clone() for t in g.opt.states() + [g.opt.x_outer, g.opt.x_outer_mom]]
+    assert g.opt.sync(1) == 1
+    mask, stats = g.opt.sync_stats(1) if K <= 16 else (1, None)
+    assert mask == 1
+    assert g.opt.sync(abi.MTDAO_SYNC_AUTO) & 1
+    torch.cuda.synchronize()
+    for p, q in zip(keep, g.opt.states() + [g.opt.x_outer, g.opt.x_outer_mom]):
+        assert torch.equal(p, q)
+    if w.param_dtype == "f32":
+        assert stats[0][abi.MTDAO_STAT_MEAN_SQ] == 0.0 and stats[0][abi.MTDAO_STAT_VARIANCE] == 0.0
+    o = run_oracle(w, _steps(w), outer=NESTEROV)
+    compare(w, g.opt, o, f"nesterov-repeat-{name}-{K}-{fused}")
+    free(g)
+
+
 def test_outer_nesterov_unit_lr_is_averaging():
     """outer_lr = 1, momentum 0 restarts every worker from the mean."""
     w = synth.small_variant(synth.WORKLOADS["sgdm_n2_k16_p354m_clip"], 30_000).replace(steps=48)
@@ -564,11 +673,10 @@ def test_outer_nesterov_full_size_bench_workload():
     w = synth.WORKLOADS["adam_n3_k4_p1311m"].replace(steps=128)
     idx = synth.sample_indices(w)
     g = run_gpu(w, _steps(w), outer=NESTEROV, fused=True)
-    o = run_oracle(w, _steps(w), idx, outer=NESTEROV)
+    o = run_oracle_parallel(w, _steps(w), idx, outer=NESTEROV, rms_cols=synth.strided_mask(w, idx))
     assert g.masks == o.masks
-    from gpu_harness import OracleResult
-    # the outer rows are [P]; compare them on the sample too
-    compare(w, g.opt, OracleResult(o.state, o.masks, idx), "nesterov-full")
+    # the outer rows are [P]; they are compared on the same columns
+    compare(w, g.opt, o, "nesterov-full")
     free(g)
 
 
@@ -598,11 +706,12 @@ def test_sync_stats_against_oracle(name, outer, tail):
     log(f"case stats {w.name} K={w.replicas} outer={outer}")
     d = torch.device("cuda:0")
     dev = DeviceInputs(w, d)
-    from gpu_harness import gpu_config, oracle_cfg, OracleResult
+    from gpu_harness import gpu_config, oracle_cfg
     a = MtdaoOptimizer(gpu_config(w, 0, outer), d, x0=dev.x0_row())
     b = MtdaoOptimizer(gpu_config(w, 0, outer), d, x0=dev.x0_row())
     ocfg = oracle_cfg(w, outer)
     ost = oracle.new_state(ocfg, synth.host_x0_row(w), w.replicas)
+    track = XAbsMax(ost)
     gdt = torch.bfloat16 if w.grad_dtype == "bf16" else torch.float32
     grads = torch.empty((w.replicas, w.numel), dtype=gdt, device=d)
     checked = 0
@@ -614,7 +723,9 @@ def test_sync_stats_against_oracle(name, outer, tail):
         mb, stats = b.sync_stats()
         oracle.local_step(ocfg, ost, synth.host_grad_rows(w, s), s, w.lr, w.adopt_clip_value(s),
                           oracle.clip_scales(ocfg, synth.host_grad_rows(w, s)))
+        track.update(ost)
         ostats = oracle.sync_stats(ocfg, ost, oracle.schedule(ocfg, s))
+        track.update(ost)
         assert ma == mb == oracle.schedule(ocfg, s)
         for sid in range(abi.MTDAO_MAX_N + 2):
             if sid not in ostats:
@@ -634,7 +745,7 @@ def test_sync_stats_against_oracle(name, outer, tail):
         assert torch.equal(p, q)
     if outer is not None:
         assert torch.equal(a.x_outer, b.x_outer) and torch.equal(a.x_outer_mom, b.x_outer_mom)
-    compare(w, b, OracleResult(ost, [], None), f"stats-{name}")
+    compare(w, b, OracleResult(ost, [], None, x_absmax=[track.a], steps=w.steps), f"stats-{name}")
     a.close()
     b.close()
 
@@ -803,10 +914,12 @@ def test_random_probabilistic(seed):
     assert applied == masks
     ocfg = oracle.OracleConfig.from_workload(w)
     ost = oracle.new_state(ocfg, synth.host_x0_row(w), w.replicas)
-    oracle.run_probabilistic(ocfg, ost, lambda s: synth.host_grad_rows(w, s), _steps(w),
-                             lambda s: w.lr, lambda s: masks[s - 1])
-    from gpu_harness import OracleResult
-    compare(w, opt, OracleResult(ost, masks, None), f"random-prob{seed}")
+    track = XAbsMax(ost)
+    for s in _steps(w):
+        oracle.run_probabilistic(ocfg, ost, lambda s_: synth.host_grad_rows(w, s_), [s],
+                                 lambda s_: w.lr, lambda s_: masks[s_ - 1])
+        track.update(ost)
+    compare(w, opt, OracleResult(ost, masks, None, x_absmax=[track.a]), f"random-prob{seed}")
     opt.close()
     torch.cuda.empty_cache()
 
