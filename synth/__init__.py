@@ -18,10 +18,12 @@ from .workloads import (  # noqa: F401
     grad_pool,
     x_pool,
     host_grad_rows,
+    host_grad_range,
     host_pool_rows,
     host_x0_row,
     f32_to_bf16_bits,
     bf16_bits_to_f32,
     sample_indices,
+    strided_mask,
     bernoulli_masks,
 )

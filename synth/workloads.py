@@ -293,6 +293,42 @@ def host_grad_rows(w: Workload, step: int, idx: Optional[np.ndarray] = None) -> 
     return rows
 
 
+def _rotated_into(pool: np.ndarray, start: int, out: np.ndarray) -> None:
+    """out[k] = pool[(start + k) mod POOL_SIZE], copied as contiguous runs."""
+    n, pos, j = out.size, 0, start % POOL_SIZE
+    while pos < n:
+        take = min(n - pos, POOL_SIZE - j)
+        out[pos:pos + take] = pool[j:j + take]
+        pos += take
+        j = 0
+
+
+def host_grad_range(w: Workload, step: int, lo: int, hi: int) -> np.ndarray:
+    """host_grad_rows(w, step, arange(lo, hi)), built from contiguous runs of
+    the pool and one fp32 multiply per tensor segment (the same exactly
+    rounded products), for long contiguous element ranges."""
+    n = hi - lo
+    pool = grad_pool(w)
+    sig = w.tensor_sigmas()
+    offs = w.tensor_offsets()
+    first = int(np.searchsorted(offs, lo, side="right")) - 1
+    segs = []
+    t = max(first, 0)
+    while t < len(w.tensors) and offs[t] < hi:
+        a, b = max(int(offs[t]), lo), min(int(offs[t + 1]), hi)
+        if b > a:
+            segs.append((a - lo, b - lo, sig[t]))
+        t += 1
+    rows = np.empty((w.replicas, n), dtype=np.float32)
+    for m in range(w.replicas):
+        _rotated_into(pool, lo + grad_offset(w.seed_g, m, step), rows[m])
+        for a, b, sg in segs:
+            np.multiply(rows[m, a:b], sg, out=rows[m, a:b])
+    if w.grad_dtype == "bf16":
+        return f32_to_bf16_bits(rows)
+    return rows
+
+
 def host_pool_rows(w: Workload, stream: int, scale: float, idx: np.ndarray, absolute: bool = False,
                    dtype: str = "f32") -> np.ndarray:
     """Seeded per-worker fields for resume tests (initial moments or
@@ -323,10 +359,14 @@ def host_x0_row(w: Workload, idx: Optional[np.ndarray] = None) -> np.ndarray:
     return row
 
 
-def sample_indices(w: Workload, n_stride: int = 1 << 16, edge: int = 64) -> np.ndarray:
+def sample_indices(w: Workload, n_stride: int = 1 << 20, edge: int = 64) -> np.ndarray:
     """Deterministic element subsample: the first and last ``edge`` elements
-    of every tensor plus ``n_stride`` evenly strided elements and the last
-    element overall, sorted and unique (int64)."""
+    of every tensor, ``n_stride`` evenly strided elements (strided_mask marks
+    them: an unbiased subset), the last element overall, and ``edge``
+    columns on either side of every column where a flat element index
+    m P + i or a flat byte offset of an fp32 or bf16 buffer reaches 2^31,
+    2^32 or 2^33 (where 32-bit index arithmetic would wrap).  Sorted and
+    unique (int64)."""
     offs = w.tensor_offsets()
     parts = []
     for a, b in zip(offs[:-1], offs[1:]):
@@ -336,7 +376,21 @@ def sample_indices(w: Workload, n_stride: int = 1 << 16, edge: int = 64) -> np.n
     stride = max(1, P // max(1, n_stride))
     parts.append(np.arange(0, P, stride, dtype=np.int64)[:n_stride])
     parts.append(np.array([P - 1]))
+    for flat in sorted({1 << k for k in (29, 30, 31, 32, 33)}):
+        for m in range(w.replicas):
+            c = flat - m * P
+            if 0 <= c < P:
+                parts.append(np.arange(max(0, c - edge), min(P, c + edge)))
     return np.unique(np.concatenate(parts).astype(np.int64))
+
+
+def strided_mask(w: Workload, idx: np.ndarray, n_stride: int = 1 << 20) -> np.ndarray:
+    """Which entries of a sample_indices(w, n_stride) sample are its evenly
+    strided elements: a subset whose statistics (an rms) are those of the
+    whole row, unlike the tensor edges, where the short norm vectors are
+    over-represented."""
+    stride = max(1, w.numel // max(1, n_stride))
+    return (idx % stride == 0) & (idx // stride < n_stride)
 
 
 def bernoulli_masks(seed: int, steps: int, n_moments: int, p_x: float, p_u: Sequence[float],
