@@ -5,18 +5,25 @@ One step = one pass of the whole hot path over one batch of synthetic
 gradients: the per-replica clip norm (when the workload clips), the fused
 local step of every replica, and the replica-mean of every state the
 schedule makes due at that step -- one mtdao_step_sync call, which folds
-the averaging into the step's pass on steps where states are due.  Inputs (states and one filled gradient
-buffer) are resident in HBM before the timed region.  The default run times
-256 consecutive steps of the 1.31B-parameter, K=4, Adam N=3 fp32 workload,
-so the timed window holds exactly the amortised share of syncs (x: 4,
-each u^j: 2, v: 1).
+the averaging into the step's pass on steps where states are due.  Inputs
+(states and one filled gradient buffer) are resident in HBM before the timed
+region.  The default run times 256 consecutive steps of the 1.31B-parameter,
+K=4, Adam N=3 fp32 workload.  The window is centred on the step at which
+every state is due together (s = 256 for that workload), so it holds that
+averaging event at any --steps, and at 256 steps the amortised share of
+every state's events (x: 4, each u^j: 2, v: 1).
 
 Prints ONE JSON line.  Extra objects:
   step / sync       element-updates/s and GB/s of each part, % of HBM peak
                     (step: mean and median of the timed launches with nothing
                     due; sync: the standalone averaging pass per state, median
-                    of 20 launches outside the timed region; step_sync_fused:
-                    the fused launches of the window)
+                    of 20 launches outside the timed region)
+  step_sync_fused   the fused step + averaging: the window's launches with
+                    due states, and 10 launches each with x due and with
+                    every state due, outside the window
+  achievable        plain copy / read / write kernels, and a bare stream
+                    with the step's exact access mix on the same buffers
+  device            the device the line was measured on
   roofline          dominant kernel (the local step): algorithmic bytes per
                     launch / mean launch time from HIP events on its stream
   cpu_baseline      the CPU oracle, unchanged, on a bounded sample of the same
@@ -85,7 +92,35 @@ def stream_lib():
         getattr(L, n).restype = ctypes.c_int32
     L.stream_ref_fill.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p]
     L.stream_ref_fill.restype = ctypes.c_int32
+    L.stream_ref_step_mix.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.POINTER(ctypes.c_void_p),
+                                      ctypes.c_int32, ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32,
+                                      ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p]
+    L.stream_ref_step_mix.restype = ctypes.c_int32
     return L
+
+
+def same_mix(opt, grads, w, stream, reps: int = 10) -> float:
+    """Seconds per launch of a bare stream with the local step's exact access
+    mix (reads g, x, u^j, v; writes x, u^j, v back unchanged) on the
+    optimizer's own buffers, with the step kernel's tile placement and
+    windows: the ceiling the step is measured against."""
+    import ctypes
+
+    import torch
+
+    L = stream_lib()
+    u = (ctypes.c_void_p * len(opt.u))(*[t.data_ptr() for t in opt.u])
+    args = (opt.x.data_ptr(), grads.data_ptr(), u, len(opt.u), opt.v.data_ptr() if opt.v is not None else None,
+            int(w.param_dtype == "bf16"), int(w.grad_dtype == "bf16"), w.numel, w.replicas, stream.cuda_stream)
+
+    def launch():
+        r = L.stream_ref_step_mix(*args)
+        if r != 0:
+            raise RuntimeError(f"stream_ref_step_mix: HIP error {r}")
+
+    ms = _event_times(launch, reps, stream)
+    torch.cuda.synchronize()
+    return _median(ms) / 1e3
 
 
 def _median(xs):
@@ -255,6 +290,29 @@ def calibrate_copy(nbytes: int, reps: int) -> None:
                       "GBps_read_plus_write": 2 * n4 * 16 / dt / 1e9}), flush=True)
 
 
+def _event_times(fn, reps: int, stream) -> list:
+    """Milliseconds of each of ``reps`` calls of fn (which enqueues on
+    ``stream``), HIP events around each call; one untimed call first."""
+    import torch
+
+    fn()
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+    for a, b in evs:
+        a.record(stream)
+        fn()
+        b.record(stream)
+    torch.cuda.synchronize()
+    return [a.elapsed_time(b) for a, b in evs]
+
+
+def device_info() -> dict:
+    import torch
+
+    p = torch.cuda.get_device_properties(0)
+    return {"name": p.name, "gcnArchName": getattr(p, "gcnArchName", None),
+            "compute_units": p.multi_processor_count, "memory_GB": round(p.total_memory / 1e9, 1)}
+
+
 def _time_calls(fn, reps: int, stream) -> float:
     """Mean seconds per call of fn (enqueues on ``stream``), HIP events
     around each call; one untimed call first."""
@@ -321,6 +379,8 @@ def measure_row(args) -> int:
     xs = 2 if w.param_dtype == "bf16" else 4
     eb = step_bytes_per_element(w)
     step_bytes = K * P * eb
+    # the plain call also runs the clip-norm pass when the workload clips
+    plain_bytes = K * P * (eb + norm_bytes_per_element(w))
     mean_bytes = [2 * K * xs * P] + [2 * K * 4 * P] * (w.n_moments + (1 if w.has_v else 0))
     for _ in range(args.warmup):
         opt.step_sync(grads, w.lr, w.adopt_clip_value(2), 0)
@@ -358,11 +418,29 @@ def measure_row(args) -> int:
                            "k_sgdm_averaged_momenta_waves (K <= 16)", ceil["copy_GBps"]))
     opt.close()
     out = {"row": args.row, "workload": w.name, "replicas": K, "params_per_replica": P, "form": w.form,
-           "reps": reps, "plain_step": _part("plain local step, same buffers", plain_s, step_bytes, "k_local_step",
+           "reps": reps, "plain_step": _part("plain local step, same buffers", plain_s, plain_bytes,
+                                             "k_local_step" + (" + clip-norm pass" if plain_bytes > step_bytes else ""),
                                              ceil["copy_GBps"]),
+           "device": device_info(),
            "parts": parts, "achievable": ceil, "peak_GBps": HBM_PEAK_GBS}
     print(json.dumps(out), flush=True)
     return 0
+
+
+def window_start(w, steps: int, warmup: int) -> int:
+    """Updates applied before the warm-up, so that the timed window of
+    ``steps`` steps is centred on the first step at which every state is
+    due together (the least common multiple of the periods): whatever
+    --steps is, the window holds that all-states averaging event, and for
+    a window of one such period the amortised share of every state's
+    events.  Kept at >= 0; the updates themselves are not run."""
+    periods = [h for h in (w.period_x, *w.period_u, w.period_v if w.has_v else 0) if h > 0]
+    if not periods:
+        return 0
+    lcm = 1
+    for h in periods:
+        lcm = lcm * h // math.gcd(lcm, h)
+    return max(0, lcm - (steps + 1) // 2 - warmup)
 
 
 def main() -> int:
@@ -372,6 +450,9 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=8)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--grad-in-arena", type=int, choices=[0, 1], default=1,
+                    help="1: the gradient rows are carved from the optimizer's own allocation (default); "
+                         "0: a separate torch allocation")
     ap.add_argument("--row", choices=["step", "outer", "stats", "prob"], default="step",
                     help="step: the hot path (the default line); outer / stats / prob: the kernels of the "
                          "Nesterov OuterOpt, the averaging diagnostics, Algorithm 4's step (--steps = reps)")
@@ -400,28 +481,32 @@ def main() -> int:
     w = synth.WORKLOADS[args.workload]
     d = torch.device("cuda:0")
     K, P = w.replicas, w.numel
-    print(f"bench: {w.name} K={K} P={P} warmup={args.warmup} steps={args.steps}", file=sys.stderr,
-          flush=True)
+    start = window_start(w, args.steps, args.warmup)
+    print(f"bench: {w.name} K={K} P={P} warmup={args.warmup} steps={args.steps} "
+          f"window s={start + args.warmup + 1}..{start + args.warmup + args.steps}", file=sys.stderr, flush=True)
     dev = DeviceInputs(w, d)
-    cfg = abi.config_from_workload(w)
-    opt = MtdaoOptimizer(cfg, d, x0=dev.x0_row())
-    gdt = torch.bfloat16 if w.grad_dtype == "bf16" else torch.float32
-    grads = torch.empty((K, P), dtype=gdt, device=d)
+    cfg = abi.config_from_workload(w, start_step=start)
+    opt = MtdaoOptimizer(cfg, d, x0=dev.x0_row(), grad_buffer=bool(args.grad_in_arena))
+    if args.grad_in_arena:
+        grads = opt.grad
+    else:
+        gdt = torch.bfloat16 if w.grad_dtype == "bf16" else torch.float32
+        grads = torch.empty((K, P), dtype=gdt, device=d)
     dev.grads_into(1, grads)
     del dev
     torch.cuda.synchronize()
     stream = torch.cuda.current_stream()
 
-    def one_step(s, ev=None):
+    def one_step(s, ev=None, mask=abi.MTDAO_SYNC_AUTO):
         # local step of every replica + averaging of the states due at s, one call
         if ev is not None:
             ev[0].record(stream)
-        applied = opt.step_sync(grads, w.lr, w.adopt_clip_value(s))
+        applied = opt.step_sync(grads, w.lr, w.adopt_clip_value(s), mask)
         if ev is not None:
             ev[1].record(stream)
         return applied
 
-    s = 0
+    s = start
     for _ in range(args.warmup):
         s += 1
         one_step(s)
@@ -447,38 +532,62 @@ def main() -> int:
     # the dominant kernel: the local step on steps with nothing due
     step_launch_s = (sum(plain) / len(plain) if plain else sum(call_ms) / len(call_ms)) / 1e3
 
+    # outside the timed window: the fused step + averaging with x due, and
+    # with every state due (10 launches each), then the same-mix bare stream
+    nstates = 1 + w.n_moments + (1 if w.has_v else 0)
+    fused_masks = {"x": 1, "all_states": (1 << nstates) - 1}
+    fused_extra = {}
+    for label, fm in fused_masks.items():
+        def call(fm=fm):
+            nonlocal s
+            s += 1
+            one_step(s, mask=fm)
+        ms = _event_times(call, 10, stream)
+        fused_extra[label] = ms
+    mix_s = same_mix(opt, grads, w, stream)
+
     # per-state sync time (replica mean of one state), untimed region: the
     # median of 20 launches, each bracketed by its own events
-    nstates = 1 + w.n_moments + (1 if w.has_v else 0)
     sync_s = []
     for sid in range(nstates):
-        opt.sync(1 << sid)
-        sev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(20)]
-        for a, b in sev:
-            a.record(stream)
-            opt.sync(1 << sid)
-            b.record(stream)
-        torch.cuda.synchronize()
-        sync_s.append(_median([a.elapsed_time(b) for a, b in sev]) / 1e3)
+        sync_s.append(_median(_event_times(lambda sid=sid: opt.sync(1 << sid), 20, stream)) / 1e3)
     opt.close()
     del opt, grads
     torch.cuda.empty_cache()
     ceil = achievable()
 
-    eb = step_bytes_per_element(w) + norm_bytes_per_element(w)
+    eb_step = step_bytes_per_element(w)
+    eb = eb_step + norm_bytes_per_element(w)
     # the timed call: the local step, preceded by the clip-norm pass when
     # clipping is on (its bytes are then part of the call's algorithmic bytes)
     launch_bytes = K * P * eb
     roof_kernel = "k_local_step" if norm_bytes_per_element(w) == 0 else \
         "k_sumsq_partial + k_clip_finalize + k_local_step"
     step_gbs = K * P * eb / step_launch_s / 1e9
+    ceil["same_mix_GBps"] = K * P * eb_step / mix_s / 1e9
+    ceil["same_mix_note"] = ("bare stream with the step's reads and writes (no arithmetic) on the same buffers, "
+                             "same tile placement and windows; median of 10 launches")
     sync_report = []
     names = ["x"] + [f"u{j + 1}" for j in range(w.n_moments)] + (["v"] if w.has_v else [])
     for sid, t in enumerate(sync_s):
         es = 2 if (sid == 0 and w.param_dtype == "bf16") else 4
         gbs = 2 * K * es * P / t / 1e9
-        sync_report.append({"state": names[sid], "ms": t * 1e3, "GBps": gbs, "pct_hbm_peak": 100 * gbs / HBM_PEAK_GBS})
+        sync_report.append({"state": names[sid], "ms": t * 1e3, "GBps": gbs, "pct_hbm_peak": 100 * gbs / HBM_PEAK_GBS,
+                            "pct_of_plain_copy": 100 * gbs / ceil["copy_GBps"]})
 
+    def fused_entry(ms_list, what):
+        mean = sum(ms_list) / len(ms_list)
+        gbs = launch_bytes / (mean / 1e3) / 1e9
+        return {"launches": len(ms_list), "mean_ms": mean, "median_ms": _median(ms_list), "GBps": gbs,
+                "pct_hbm_peak": 100 * gbs / HBM_PEAK_GBS,
+                "over_plain_step_pct": 100 * (mean / 1e3 / step_launch_s - 1), "note": what}
+
+    step_sync_fused = {
+        "in_window": fused_entry(fused, "the window's steps with due states") if fused else {"launches": 0},
+        "x_due": fused_entry(fused_extra["x"], "outside the window: mtdao_step_sync with x due"),
+        "all_states_due": fused_entry(fused_extra["all_states"],
+                                      "outside the window: mtdao_step_sync with every state due"),
+    }
     value = K * P * args.steps / wall
     traffic = load_traffic(w.name, launch_bytes)
     out = {
@@ -497,19 +606,21 @@ def main() -> int:
         "config": {"workload": w.name, "replicas": K, "params_per_replica": P, "form": w.form,
                    "n_moments": w.n_moments, "param_dtype": w.param_dtype, "grad_dtype": w.grad_dtype,
                    "periods": {"x": w.period_x, "u": list(w.period_u), "v": w.period_v},
-                   "syncs_in_window": {str(k): v for k, v in sorted(syncs.items())}},
+                   "window_steps": [start + args.warmup + 1, start + args.warmup + args.steps],
+                   "syncs_in_window": {str(k): v for k, v in sorted(syncs.items())},
+                   "grad_in_arena": bool(args.grad_in_arena)},
+        "device": device_info(),
         "step": {"mean_launch_ms": step_launch_s * 1e3,
                  "median_launch_ms": _median(plain if plain else call_ms),
+                 "launches": len(plain),
                  "element_updates_per_s": K * P / step_launch_s,
                  "bytes_per_element_update": eb, "GBps": step_gbs,
                  "pct_hbm_peak": 100 * step_gbs / HBM_PEAK_GBS,
-                 "pct_of_plain_copy": 100 * step_gbs / ceil["copy_GBps"]},
+                 "pct_of_plain_copy": 100 * step_gbs / ceil["copy_GBps"],
+                 "pct_of_same_mix": 100 * (K * P * eb_step / step_launch_s) / (K * P * eb_step / mix_s)},
         "achievable": ceil,
         "sync": sync_report,
-        "step_sync_fused": {"launches": len(fused),
-                            "mean_ms": (sum(fused) / len(fused)) if fused else None,
-                            "GBps": (K * P * eb / (sum(fused) / len(fused) / 1e3) / 1e9) if fused else None,
-                            "note": "steps with due states: local step and averaging in one pass, same bytes as the step"},
+        "step_sync_fused": step_sync_fused,
         "roofline": {"bound": "hbm", "achieved": launch_bytes / step_launch_s / 1e9, "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": launch_bytes / step_launch_s / 1e9 / HBM_PEAK_GBS,
                      "traffic": traffic, "kernel": roof_kernel,

@@ -26,12 +26,15 @@ class MtdaoOptimizer:
 
     ``x0``: [P] initial parameters (broadcast to every replica), or, with
     ``resume=True``, full [K][P] states ``x``, ``u`` (list of N) and ``v``
-    that are taken as they are (e.g. read back from a checkpoint)."""
+    that are taken as they are (e.g. read back from a checkpoint).
+    ``grad_buffer``: also carve a [K][P] gradient buffer (``grad``) from the
+    states' allocation, for callers that fill gradients in place."""
 
     def __init__(self, cfg: abi.MtdaoConfig, device: torch.device, x0: Optional[torch.Tensor] = None,
                  resume: bool = False, x: Optional[torch.Tensor] = None,
                  u: Optional[List[torch.Tensor]] = None, v: Optional[torch.Tensor] = None,
-                 x_outer: Optional[torch.Tensor] = None, x_outer_mom: Optional[torch.Tensor] = None):
+                 x_outer: Optional[torch.Tensor] = None, x_outer_mom: Optional[torch.Tensor] = None,
+                 grad_buffer: bool = False):
         self.cfg = cfg
         K, P, N = cfg.replicas, cfg.numel, cfg.n_moments
         self.K, self.P, self.N = K, P, N
@@ -40,6 +43,7 @@ class MtdaoOptimizer:
         nesterov = cfg.outer_opt == abi.MTDAO_OUTER_NESTEROV
         self.x_outer = self.x_outer_mom = None
         self._arena = None
+        self.grad: Optional[torch.Tensor] = None
         if resume:
             assert x is not None and u is not None and len(u) == N
             assert (v is not None) == self.has_v
@@ -51,7 +55,11 @@ class MtdaoOptimizer:
             shapes = [((K, P), xdt)] + [((K, P), torch.float32)] * (N + (1 if self.has_v else 0))
             if nesterov:
                 shapes += [((P,), torch.float32)] * 2
+            if grad_buffer:
+                shapes.append(((K, P), _TORCH_DTYPE[cfg.grad_dtype]))
             views = self._carve(shapes, device)
+            if grad_buffer:
+                self.grad = views.pop()
             self.x, self.u = views[0], views[1:1 + N]
             self.v = views[1 + N] if self.has_v else None
             if nesterov:
