@@ -23,7 +23,11 @@ import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "mtdao_oracle.c")
-_LIB = os.path.join(_HERE, "_liboracle.so")
+# MTDAO_ORACLE_SANITIZE=1 selects a build with AddressSanitizer and
+# UndefinedBehaviorSanitizer (load it with gcc's libasan preloaded).
+SANITIZE = os.environ.get("MTDAO_ORACLE_SANITIZE") == "1"
+SAN_FLAGS = ["-fsanitize=address,undefined", "-fno-sanitize-recover=all", "-fno-omit-frame-pointer", "-g"]
+_LIB = os.path.join(_HERE, "_liboracle_san.so" if SANITIZE else "_liboracle.so")
 
 MAX_N = 4
 F32, BF16, F64 = 0, 1, 2
@@ -36,10 +40,11 @@ _NP_DTYPE = {F32: np.float32, BF16: np.uint16, F64: np.float64}
 
 
 def build(force: bool = True) -> str:
-    """Compile the oracle with gcc (no fast-math, no FMA contraction)."""
+    """Compile the oracle with gcc (no fast-math, no FMA contraction; with
+    the sanitizers when MTDAO_ORACLE_SANITIZE=1)."""
     if force or not os.path.exists(_LIB):
         cmd = ["gcc", "-O2", "-std=c11", "-ffp-contract=off", "-fno-fast-math", "-fPIC", "-shared",
-               "-Wall", "-Wextra", "-o", _LIB + ".tmp", _SRC, "-lm"]
+               "-Wall", "-Wextra", *(SAN_FLAGS if SANITIZE else []), "-o", _LIB + ".tmp", _SRC, "-lm"]
         subprocess.run(cmd, check=True)
         os.replace(_LIB + ".tmp", _LIB)
     return _LIB

@@ -104,8 +104,8 @@ def test_mutant_is_caught(mutant, workdir):
     so = os.path.join(workdir, f"{name}.so")
     with open(src, "w") as f:
         f.write(_mutate(name, old, new, occ))
-    subprocess.run(["gcc", "-O2", "-std=c11", "-ffp-contract=off", "-fPIC", "-shared", "-o", so, src,
-                    "-lm"], check=True)
+    subprocess.run(["gcc", "-O2", "-std=c11", "-ffp-contract=off", "-fPIC", "-shared",
+                    *(oracle.SAN_FLAGS if oracle.SANITIZE else []), "-o", so, src, "-lm"], check=True)
     oracle.use_library(so)
     try:
         for pin in oracle_pins.ALL_PINS:
