@@ -29,27 +29,33 @@ from synth.device import DeviceInputs
 #  fp32 states: max_i |a_i - b_i| / max(|b_i|, rms(b)) <= 1e-5, rms over an
 #  unbiased subset of the row.
 #  bf16 params: |a - b| in bf16 ulps at max(largest |x| of the element's
-#  trajectory, rms(b)) (XAbsMax).  The kernel rounds its fp32 value and the
-#  oracle its fp64 value to bf16; when the exact value lies within the fp32
-#  error of a rounding boundary the two pick neighbours one ulp apart, and
-#  that offset persists (x feeds every later update).  Each such flip adds
-#  at most one unit, so: at most BF16_MAX_ULPS units anywhere; at most
-#  BF16_FLIP_RATE * T * n + BF16_SLACK elements (n compared, T steps) one
-#  unit or more apart, and at most (BF16_FLIP_RATE * T)^2 * n + BF16_SLACK
-#  more than one unit apart (two flips on one element).
+#  trajectory, rms(b)) times BF16_HEADROOM (XAbsMax).  The kernel rounds its
+#  fp32 value and the oracle its fp64 value to bf16; when the exact value
+#  lies within the fp32 error of a rounding boundary the two pick neighbours
+#  one ulp apart (a flip), and that offset persists (x feeds every later
+#  update).  An averaging of x carries a flip of one worker into the mean,
+#  shifted by ulp/K, so it can move the rounded mean, and with it all K
+#  workers, by one ulp.  Each such event adds at most one unit; three in
+#  the same direction on one element are the most the 124M x 8 workload
+#  shows over 128 steps (2.3e-4 of the elements >= 1 unit, 7.8e-6 > 1).
+#  Bounds: at most BF16_MAX_ULPS units anywhere; at most
+#  2 BF16_FLIP_RATE T n + BF16_SLACK elements (n compared, T steps; the 2
+#  for the flips the averaging carries to other workers) one unit or more
+#  apart, and at most a tenth of that (plus the slack) more than one unit.
 REL_TOL = 1e-5
-BF16_MAX_ULPS = 2
-BF16_FLIP_RATE = 1e-5   # per element and step, against ~3.5e-6 measured
-BF16_SLACK = 4          # elements, for small comparisons
+BF16_MAX_ULPS = 3
+BF16_HEADROOM = 1.0 + 2.0 ** -5  # 4 ulps: how far the two trajectories may be apart
+BF16_FLIP_RATE = 1e-5   # per element and step, against 2e-6 measured on 124M x 8 over 128 steps
+BF16_SLACK = 32         # elements, for small comparisons
 BF16_OUTER_MAX_ULPS = 16  # >= lr (1 + mu) / (1 - mu) = 13.3 for the tested (0.7, 0.9)
-BF16_OUTER_FRAC = 2e-2
+BF16_OUTER_FRAC = 1e-2  # 3.4e-3 measured over 96 steps
 
 
 def bf16_bounds(n: float, steps: int):
     """(most elements >= 1 unit apart, most elements > 1 unit apart) for n
     compared bf16 values after ``steps`` steps."""
-    r = BF16_FLIP_RATE * max(1, steps)
-    return r * n + BF16_SLACK, r * r * n + BF16_SLACK
+    r = 2 * BF16_FLIP_RATE * max(1, steps)
+    return r * n + BF16_SLACK, 0.1 * r * n + BF16_SLACK
 
 
 def log(msg: str) -> None:
@@ -348,7 +354,11 @@ def _metrics(kind: str, a: np.ndarray, b: np.ndarray, rms: float, ref: Optional[
         nz = bf != 0
         out["rel_err_unfloored"] = float((d[nz] / np.abs(bf[nz])).max(initial=0.0))
     elif kind == "bf16":
-        ul = d / ulp_unit(np.maximum(np.maximum(np.abs(bf), ref.astype(np.float64)), rms))
+        # the kernel's trajectory stays within a few ulps of the oracle's, so
+        # it may cross into the next binade where the oracle's largest
+        # magnitude lies just below one: units at BF16_HEADROOM times it
+        scale = np.maximum(np.maximum(np.abs(bf), ref.astype(np.float64)), rms) * BF16_HEADROOM
+        ul = d / ulp_unit(scale)
         out.update(max_ulps=float(ul.max(initial=0.0)), n_ge1=float((ul >= 1).sum()), n_gt1=float((ul > 1).sum()),
                    rel_err=float((d / np.maximum(np.maximum(np.abs(bf), rms), 1e-300)).max(initial=0.0)))
     else:  # measured at the scale of the outer parameters (ref)
@@ -477,11 +487,10 @@ def compare(w: synth.Workload, gpu: MtdaoOptimizer, orc: OracleResult, label: st
                 # outer parameters, the affected fraction by the flip rate.
                 assert m["max_ulps_of_x"] <= BF16_OUTER_MAX_ULPS and frac_off <= BF16_OUTER_FRAC, (label, name, m)
             else:
-                # b sums outer gradients d = x_outer - E_m[x^m], |d| << |x|: an
-                # error of 1e-5 |x| in the operands becomes up to 2e-5 |x| in d
-                # and, summed over ~1/(1 - mu) events, 2e-5 |x| / (1 - mu) in b.
-                tol = 2 * REL_TOL / (1 - float(gpu.cfg.outer_momentum))
-                assert m["err_of_x_outer"] <= tol, (label, name, m, tol)
+                # b sums outer gradients d = x_outer - E_m[x^m] with |d| << |x|,
+                # so its fp32 rounding errors are those of x-scale operands: it
+                # is held to the 1e-5 bound at the scale of the outer parameters
+                assert m["err_of_x_outer"] <= REL_TOL, (label, name, m)
             worst[name + "_of_x_outer"] = m["err_of_x_outer"]
     REPORT.append((label, worst))
     return report
