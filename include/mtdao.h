@@ -253,6 +253,23 @@ int32_t mtdao_stats_scratch_bytes(const mtdao_config* cfg, size_t* bytes);
 int32_t mtdao_sync_stats(mtdao_handle* h, uint32_t mask, uint32_t* applied_mask, void* scratch, size_t scratch_bytes,
                          double* host_stats, void* hip_stream);
 
+/* mtdao_sync_stats without a caller scratch buffer, for callers that
+ * cannot allocate device memory (serving loops and harnesses that forbid
+ * allocation).  The partial sums live in a static device array of
+ * MTDAO_STATIC_SCRATCH_BYTES that every GPU the library runs on holds until
+ * the process ends, shared by all calls on that GPU: calls that overlap on
+ * one GPU (other streams, other threads, other handles) race and must be
+ * serialised by the caller.  Every scratch word a call reads is written
+ * earlier in the same call, so nothing is cleared between calls.  Same
+ * results as mtdao_sync_stats, bit for bit.  MTDAO_ERR_WORKSPACE (nothing
+ * enqueued) when mtdao_stats_scratch_bytes exceeds the static size, about
+ * K P (N + 2)(3 + 2K) / 128 bytes: e.g. up to 156M parameters at K = 4,
+ * N = 3.  The handle's device must be current.  Calls no allocator; waits
+ * for the stream. */
+#define MTDAO_STATIC_SCRATCH_BYTES (64u << 20)
+int32_t mtdao_sync_stats_static(mtdao_handle* h, uint32_t mask, uint32_t* applied_mask, double* host_stats,
+                                void* hip_stream);
+
 /* The schedule alone: states due after update s for this configuration.
  * Host-only; no GPU needed. */
 int32_t mtdao_schedule(const mtdao_config* cfg, int64_t s, uint32_t* mask);

@@ -9,6 +9,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <type_traits>
 #include <vector>
@@ -738,6 +739,37 @@ int32_t mtdao_sync(mtdao_handle* h, uint32_t mask, uint32_t* applied_mask, void*
 
 namespace {
 
+// Device scratch of mtdao_sync_stats_static, for callers that cannot
+// allocate device memory: one array per GPU for the life of the process,
+// shared by every call on that GPU.  In host code `scratch` only names the
+// symbol; its device address comes from hipGetSymbolAddress, once per
+// device, with that device current.
+constexpr size_t kStaticScratchDoubles = MTDAO_STATIC_SCRATCH_BYTES / sizeof(double);
+__device__ __align__(256) double scratch[kStaticScratchDoubles];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mutex;
+double* g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of this device's `scratch`, looked up on first use.
+int32_t static_scratch(mtdao_handle* h, double** out) {
+  int dev = -1;
+  int32_t r = hip_check(&h->err, hipGetDevice(&dev), "hipGetDevice");
+  if (r != MTDAO_OK) return r;
+  if (dev < 0 || dev >= kMaxDevices)
+    return fail(&h->err, MTDAO_ERR_INVALID_ARG, "device %d outside [0, %d)", dev, kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mutex);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    r = hip_check(&h->err, hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)), "hipGetSymbolAddress(scratch)");
+    if (r != MTDAO_OK) return r;
+    if (!p) return fail(&h->err, MTDAO_ERR_HIP, "hipGetSymbolAddress(scratch) gave NULL");
+    g_scratch_ptr[dev] = reinterpret_cast<double*>(p);
+  }
+  *out = g_scratch_ptr[dev];
+  return MTDAO_OK;
+}
+
 // Checks shared by both diagnostics entry points (before any scratch check).
 int32_t check_stats_args(mtdao_handle* h, double* host_stats) {
   const mtdao_config& c = h->cfg;
@@ -834,6 +866,23 @@ int32_t mtdao_sync_stats(mtdao_handle* h, uint32_t mask, uint32_t* applied_mask,
     return fail(&h->err, MTDAO_ERR_ALIGN, "stats scratch is not 256-byte aligned");
   return run_sync_stats(h, mask, applied_mask, reinterpret_cast<double*>(scratch), host_stats,
                         reinterpret_cast<hipStream_t>(hip_stream));
+}
+
+int32_t mtdao_sync_stats_static(mtdao_handle* h, uint32_t mask, uint32_t* applied_mask, double* host_stats,
+                                void* hip_stream) {
+  if (!h) return fail(&g_err, MTDAO_ERR_INVALID_ARG, "handle is NULL");
+  int32_t r = check_stats_args(h, host_stats);
+  if (r != MTDAO_OK) return r;
+  const size_t need = stats_scratch_for(h->cfg);
+  if (need > MTDAO_STATIC_SCRATCH_BYTES)
+    return fail(&h->err, MTDAO_ERR_WORKSPACE,
+                "the diagnostics of this configuration need %zu bytes of scratch; the static scratch holds %zu "
+                "(use mtdao_sync_stats with a caller buffer)",
+                need, (size_t)MTDAO_STATIC_SCRATCH_BYTES);
+  double* sc = nullptr;
+  r = static_scratch(h, &sc);
+  if (r != MTDAO_OK) return r;
+  return run_sync_stats(h, mask, applied_mask, sc, host_stats, reinterpret_cast<hipStream_t>(hip_stream));
 }
 
 int32_t mtdao_step_sync(mtdao_handle* h, const void* grads, float lr, float adopt_clip, uint32_t mask,

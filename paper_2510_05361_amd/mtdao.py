@@ -36,6 +36,7 @@ MTDAO_ERR_ALIGN = -2
 MTDAO_ERR_HIP = -3
 MTDAO_ERR_RANGE = -4
 MTDAO_ERR_WORKSPACE = -5
+MTDAO_STATIC_SCRATCH_BYTES = 64 << 20
 
 FORMS = {"adam": MTDAO_ADAM, "adopt": MTDAO_ADOPT, "sgdm": MTDAO_SGDM}
 DTYPES = {"f32": MTDAO_F32, "bf16": MTDAO_BF16}
@@ -95,6 +96,8 @@ def lib() -> ctypes.CDLL:
         L.mtdao_stats_scratch_bytes.restype = I32
         L.mtdao_sync_stats.argtypes = [VP, U32, P(U32), VP, ctypes.c_size_t, VP, VP]
         L.mtdao_sync_stats.restype = I32
+        L.mtdao_sync_stats_static.argtypes = [VP, U32, P(U32), VP, VP]
+        L.mtdao_sync_stats_static.restype = I32
         L.mtdao_schedule.argtypes = [P(MtdaoConfig), I64, P(U32)]
         L.mtdao_schedule.restype = I32
         L.mtdao_read_state.argtypes = [VP, I32, I32, I64, I64, VP, VP]
@@ -235,6 +238,16 @@ def mtdao_sync_stats(h: int, mask: int, scratch: Optional[int], scratch_bytes: i
     out = np.empty((MTDAO_MAX_N + 2, MTDAO_STATS_STRIDE), dtype=np.float64)
     _check(lib().mtdao_sync_stats(h, int(mask) & 0xFFFFFFFF, ctypes.byref(applied), scratch, int(scratch_bytes),
                                   out.ctypes.data, stream), h)
+    return int(applied.value), out
+
+
+def mtdao_sync_stats_static(h: int, mask: int, stream: Optional[int]):
+    """mtdao_sync_stats on the library's static device scratch (no caller
+    buffer).  Returns (applied mask, stats array)."""
+    applied = ctypes.c_uint32(0)
+    out = np.empty((MTDAO_MAX_N + 2, MTDAO_STATS_STRIDE), dtype=np.float64)
+    _check(lib().mtdao_sync_stats_static(h, int(mask) & 0xFFFFFFFF, ctypes.byref(applied), out.ctypes.data,
+                                         stream), h)
     return int(applied.value), out
 
 

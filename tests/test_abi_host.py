@@ -383,11 +383,24 @@ def test_sync_stats_host_rules():
         assert applied == 0 and np.all(np.isnan(st))
     finally:
         abi.mtdao_destroy(h)
+    # the static-scratch variant rejects what its fixed array cannot hold, before anything else
+    huge = good_cfg(numel=1 << 30)
+    assert abi.mtdao_stats_scratch_bytes(huge) > abi.MTDAO_STATIC_SCRATCH_BYTES
+    h = _fake_handle(huge)
+    try:
+        with pytest.raises(abi.MtdaoError) as e:
+            abi.mtdao_sync_stats_static(h, 1, None)
+        assert e.value.code == abi.MTDAO_ERR_WORKSPACE and "static scratch" in abi.mtdao_last_error(h)
+    finally:
+        abi.mtdao_destroy(h)
     big = good_cfg(replicas=17)
     h = _fake_handle(big)
     try:
         with pytest.raises(abi.MtdaoError) as e:
             abi.mtdao_sync_stats(h, 1, 1 << 44, abi.mtdao_stats_scratch_bytes(big), None)
         assert e.value.code == abi.MTDAO_ERR_INVALID_ARG and "16" in abi.mtdao_last_error(h)
+        with pytest.raises(abi.MtdaoError) as e:
+            abi.mtdao_sync_stats_static(h, 1, None)
+        assert e.value.code == abi.MTDAO_ERR_INVALID_ARG
     finally:
         abi.mtdao_destroy(h)
