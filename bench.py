@@ -443,6 +443,75 @@ def window_start(w, steps: int, warmup: int) -> int:
     return max(0, lcm - (steps + 1) // 2 - warmup)
 
 
+def measure_graph(args) -> int:
+    """Per-step time of the 1M-parameter K=2 workload (launch-bound: its
+    75 MB sit in the MALL) three ways, one JSON line: eager mtdao_step_sync
+    calls, eager mtdao_step_sync_device calls, and replays of a HIP graph of
+    one schedule period (16 steps) of mtdao_step_sync_device, whose eta_t
+    and bias corrections are formed on the device at every replay."""
+    import numpy as np
+    import torch
+
+    import synth
+    from paper_2510_05361_amd import mtdao as abi
+    from paper_2510_05361_amd.optimizer import MtdaoOptimizer
+    from synth.device import DeviceInputs
+
+    w = synth.WORKLOADS[args.workload if args.workload != DEFAULT_WORKLOAD else "adam_n2_k2_p1m"]
+    d = torch.device("cuda:0")
+    K, P = w.replicas, w.numel
+    periods = [h for h in (w.period_x, *w.period_u, w.period_v if w.has_v else 0) if h > 0]
+    window = 1
+    for h in periods:
+        window = window * h // math.gcd(window, h)
+    reps = max(2, args.steps // window)
+    print(f"bench --row graph: {w.name} K={K} P={P} window={window} reps={reps}", file=sys.stderr, flush=True)
+    dev = DeviceInputs(w, d)
+    n_total = 2 + window * (reps + args.warmup + 2)
+    lr = torch.from_numpy(np.full(n_total, w.lr, dtype=np.float32)).to(d)
+    clip = torch.from_numpy(np.array([w.adopt_clip_value(k + 1) for k in range(n_total)], dtype=np.float32)).to(d)
+    opt = MtdaoOptimizer(abi.config_from_workload(w), d, x0=dev.x0_row(), grad_buffer=True)
+    dev.grads_into(1, opt.grad)
+    st = torch.cuda.current_stream()
+    opt.step_sync(opt.grad, w.lr, w.adopt_clip_value(1))  # update 1 (ADOPT: v only) on the host path
+
+    def eager():
+        for _ in range(window):
+            s = opt.step_count + 1
+            opt.step_sync(opt.grad, w.lr, w.adopt_clip_value(s))
+
+    opt.device_step(lr, clip if w.form == "adopt" else None)
+
+    def eager_device():
+        for _ in range(window):
+            opt.step_sync_device(opt.grad)
+
+    for _ in range(args.warmup):
+        eager()
+        eager_device()
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        eager_device()
+    torch.cuda.synchronize()
+    res = {}
+    for name, fn in (("eager_step_sync", eager), ("eager_step_sync_device", eager_device), ("graph_replay", graph.replay)):
+        if name != "eager_step_sync":
+            opt.device_step(lr, clip if w.form == "adopt" else None)
+        ms = _event_times(fn, reps, st)
+        res[name] = {"us_per_step": 1e3 * sum(ms) / len(ms) / window, "windows": reps}
+    eb = step_bytes_per_element(w) + norm_bytes_per_element(w)
+    for v in res.values():
+        v["GBps"] = K * P * eb / (v["us_per_step"] * 1e-6) / 1e9
+    del graph
+    opt.close()
+    print(json.dumps({"row": "graph", "workload": w.name, "replicas": K, "params_per_replica": P, "window_steps": window,
+                      "bytes_per_step": K * P * eb, "parts": res, "device": device_info(),
+                      "note": "per-step time includes the window's averaging events; the working set is MALL-resident, "
+                              "so this is a launch-overhead figure, not an HBM one"}), flush=True)
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -453,9 +522,10 @@ def main() -> int:
     ap.add_argument("--grad-in-arena", type=int, choices=[0, 1], default=1,
                     help="1: the gradient rows are carved from the optimizer's own allocation (default); "
                          "0: a separate torch allocation")
-    ap.add_argument("--row", choices=["step", "outer", "stats", "prob"], default="step",
+    ap.add_argument("--row", choices=["step", "outer", "stats", "prob", "graph"], default="step",
                     help="step: the hot path (the default line); outer / stats / prob: the kernels of the "
-                         "Nesterov OuterOpt, the averaging diagnostics, Algorithm 4's step (--steps = reps)")
+                         "Nesterov OuterOpt, the averaging diagnostics, Algorithm 4's step (--steps = reps); "
+                         "graph: eager and graph-replayed steps of the 1M-parameter workload")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES",
                     help="only run a plain copy of BYTES each way (counter calibration)")
     args = ap.parse_args()
@@ -468,6 +538,8 @@ def main() -> int:
     if args.calibrate_copy:
         calibrate_copy(args.calibrate_copy, max(1, args.steps))
         return 0
+    if args.row == "graph":
+        return measure_graph(args)
     if args.row != "step":
         return measure_row(args)
 

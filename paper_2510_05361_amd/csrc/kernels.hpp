@@ -222,6 +222,73 @@ __device__ __forceinline__ void outer_step_piece(const OuterParams& o, int64_t e
 
 enum StepWindows { kWinOne = 0, kWinHalves = 1, kWinPairs = 2 };
 
+// Step-dependent scalars of update s, for launches whose update number is
+// kept on the device (graph replay): k_device_step advances s and fills the
+// rest.  The layout is mtdao_device_step of the C header.
+struct DeviceStep {
+  int64_t s;           // updates applied
+  float lr;            // eta_t of update s
+  float clip;          // ADOPT c_t of update s (<= 0: no clamp)
+  float w[kMaxN];      // omega_j, times 1/(1 - beta_{1,j}^s) under bias correction
+  float inv_bc2;       // 1/(1 - beta_2^s) under bias correction, else 1
+  float reserved;
+};
+
+// b^s for s >= 0 by repeated squaring in plain IEEE double multiplies, so
+// host and device code compute the same bits.
+__host__ __device__ inline double pow_steps(double b, int64_t s) {
+#pragma clang fp contract(off)
+  double r = 1.0, a = b;
+  while (s > 0) {
+    if (s & 1) r = r * a;
+    a = a * a;
+    s >>= 1;
+  }
+  return r;
+}
+
+// Hyper-parameters the step-dependent scalars are formed from.
+struct BiasCorrection {
+  float beta[kMaxN];
+  float omega[kMaxN];
+  float beta2;
+  int32_t n;
+  int32_t on;  // Adam with bias correction
+};
+
+// w_j = omega_j / (1 - beta_j^s) and 1 / (1 - beta_2^s) (omega_j and 1
+// without correction) in double, rounded once to fp32; the same code on
+// the host (eager calls) and in k_device_step (device-side s).
+__host__ __device__ inline void step_scalars(const BiasCorrection& c, int64_t s, float* w, float* inv_bc2) {
+#pragma clang fp contract(off)
+  for (int j = 0; j < c.n; ++j)
+    w[j] = (float)(c.on ? (double)c.omega[j] / (1.0 - pow_steps((double)c.beta[j], s)) : (double)c.omega[j]);
+  *inv_bc2 = (float)(c.on ? 1.0 / (1.0 - pow_steps((double)c.beta2, s)) : 1.0);
+}
+
+// One thread: s += 1, then the scalars of update s; eta_t and c_t from
+// tables indexed by s - 1 (the last entry for s beyond the table).
+__global__ __launch_bounds__(64) void k_device_step(DeviceStep* __restrict__ d, BiasCorrection c,
+                                                   const float* __restrict__ lr_table,
+                                                   const float* __restrict__ clip_table, int64_t len) {
+  if (threadIdx.x != 0) return;
+  const int64_t s = d->s + 1;
+  const int64_t i = (s < len ? s : len) - 1;
+  float w[kMaxN] = {0.0f, 0.0f, 0.0f, 0.0f}, ib;
+  step_scalars(c, s, w, &ib);
+  d->s = s;
+  d->lr = lr_table[i];
+  d->clip = clip_table != nullptr ? clip_table[i] : 0.0f;
+#pragma unroll
+  for (int j = 0; j < kMaxN; ++j) d->w[j] = w[j];
+  d->inv_bc2 = ib;
+}
+
+// d->s = s (the other fields are filled by the next k_device_step).
+__global__ __launch_bounds__(64) void k_device_step_set(DeviceStep* __restrict__ d, int64_t s) {
+  if (threadIdx.x == 0) d->s = s;
+}
+
 // Per-launch scalars, prepared on the host in double and rounded to fp32.
 struct StepParams {
   void* x;                 // [K][P] params (XT)
@@ -243,7 +310,21 @@ struct StepParams {
   float lr;                // eta_t
   float clip;              // ADOPT c_t (<= 0: no clamp)
   OuterParams outer;       // OuterOpt applied when x is averaged
+  const DeviceStep* dev;   // non-null: lr, clip, w and inv_bc2 are read from it
 };
+
+// The launch's scalars: those of the argument block, or those of the
+// device-side step when it is given.
+__device__ __forceinline__ StepParams device_scalars(const StepParams& p0) {
+  if (p0.dev == nullptr) return p0;
+  StepParams p = p0;
+  p.lr = p0.dev->lr;
+  p.clip = p0.dev->clip;
+  p.inv_bc2 = p0.dev->inv_bc2;
+#pragma unroll
+  for (int j = 0; j < kMaxN; ++j) p.w[j] = p0.dev->w[j];
+  return p;
+}
 
 // The update of one element of one replica (the loop body of Algorithm 1, 2
 // or 3).  x, u[0..N), v hold the stored values on entry and the updated
@@ -315,7 +396,8 @@ __device__ __forceinline__ void update_element(const StepParams& p, float sc, fl
 //              window, 80.0% for halves, 80.4% for replica pairs.
 template <int FORM, int N, typename XT, typename GT, int V, int U, int NTM, int ORDER, int B = kBlock, int C = 0,
           int WIN = kWinOne>
-__global__ __launch_bounds__(B) void k_local_step(StepParams p) {
+__global__ __launch_bounds__(B) void k_local_step(StepParams p0) {
+  const StepParams p = device_scalars(p0);
   constexpr bool NTL = (NTM & 1) != 0, NTS = (NTM & 2) != 0;
 
   for (int64_t tile = blockIdx.x; tile < p.tiles; tile += gridDim.x) {
@@ -402,7 +484,8 @@ __device__ __forceinline__ float mean_of(float s0, double d, double rk) {
 // that mean to all K rows.  The separate mean pass (2 K sizeof(T) bytes
 // per element per due state) disappears.
 template <int FORM, int N, typename XT, typename GT, int V, int NTM, int ORDER, int C = 0>
-__global__ __launch_bounds__(kBlock) void k_local_step_sync(StepParams p, uint32_t mask, int32_t K) {
+__global__ __launch_bounds__(kBlock) void k_local_step_sync(StepParams p0, uint32_t mask, int32_t K) {
+  const StepParams p = device_scalars(p0);
   constexpr bool NTL = (NTM & 1) != 0, NTS = (NTM & 2) != 0;
   const bool sync_x = (mask & 1u) != 0;
   bool sync_u[N];
@@ -519,7 +602,8 @@ constexpr int kWaveMaxK = 16;
 
 template <int FORM, int N, typename XT, typename GT, int V, int NTM, int ORDER>
 __global__ __launch_bounds__(64 * kWaveMaxK) __attribute__((amdgpu_waves_per_eu(8)))
-void k_local_step_sync_waves(StepParams p, uint32_t mask, int32_t K) {
+void k_local_step_sync_waves(StepParams p0, uint32_t mask, int32_t K) {
+  const StepParams p = device_scalars(p0);
   constexpr bool NTL = (NTM & 1) != 0, NTS = (NTM & 2) != 0;
   constexpr int NS = 2 + N;  // x, u^1..u^N, v
   __shared__ float lds[kWaveMaxK][64 * V];
@@ -602,8 +686,9 @@ void k_local_step_sync_waves(StepParams p, uint32_t mask, int32_t K) {
 // same thread reloads them in pass 2) and the means of the due ones; pass 2
 // forms each replica's direction and updates x.
 template <int N, typename XT, typename GT, int V, int NTM, int C = 0>
-__global__ __launch_bounds__(kBlock) void k_sgdm_averaged_momenta(StepParams p, uint32_t mask, int32_t K) {
+__global__ __launch_bounds__(kBlock) void k_sgdm_averaged_momenta(StepParams p0, uint32_t mask, int32_t K) {
 #pragma clang fp contract(off)
+  const StepParams p = device_scalars(p0);
   constexpr bool NTL = (NTM & 1) != 0, NTS = (NTM & 2) != 0;
   const bool sync_x = (mask & 1u) != 0;
   bool sync_u[N];
@@ -713,8 +798,9 @@ __global__ __launch_bounds__(kBlock) void k_sgdm_averaged_momenta(StepParams p, 
 // pass.  Barriers are reached by every thread, also in the row tail.
 template <int N, typename XT, typename GT, int V, int NTM>
 __global__ __launch_bounds__(64 * kWaveMaxK) __attribute__((amdgpu_waves_per_eu(8)))
-void k_sgdm_averaged_momenta_waves(StepParams p, uint32_t mask, int32_t K) {
+void k_sgdm_averaged_momenta_waves(StepParams p0, uint32_t mask, int32_t K) {
 #pragma clang fp contract(off)
+  const StepParams p = device_scalars(p0);
   constexpr bool NTL = (NTM & 1) != 0, NTS = (NTM & 2) != 0;
   __shared__ float lds[kWaveMaxK][64 * V];
   const int32_t m = threadIdx.x >> 6, lane = threadIdx.x & 63;

@@ -7,6 +7,7 @@
 #include <algorithm>
 #include <cmath>
 #include <cstdarg>
+#include <cstddef>
 #include <cstdio>
 #include <cstring>
 #include <mutex>
@@ -18,6 +19,11 @@
 #include "kernels.hpp"
 
 using namespace mtdao;
+
+static_assert(sizeof(DeviceStep) == sizeof(mtdao_device_step) && offsetof(DeviceStep, lr) == offsetof(mtdao_device_step, lr) &&
+                  offsetof(DeviceStep, w) == offsetof(mtdao_device_step, w) &&
+                  offsetof(DeviceStep, inv_bc2) == offsetof(mtdao_device_step, inv_bc2),
+              "DeviceStep mirrors mtdao_device_step");
 
 struct mtdao_handle {
   mtdao_config cfg;                 // copy; tensor_numel points into `tensors`
@@ -616,9 +622,25 @@ bool claim_outer_step(mtdao_handle* h, uint32_t work, int64_t s) {
   return true;
 }
 
+BiasCorrection bias_correction_of(const mtdao_config& c) {
+  BiasCorrection b;
+  std::memset(&b, 0, sizeof b);
+  for (int j = 0; j < c.n_moments; ++j) {
+    b.beta[j] = c.beta1[j];
+    b.omega[j] = c.omega[j];
+  }
+  b.beta2 = c.beta2;
+  b.n = c.n_moments;
+  b.on = (c.form == MTDAO_ADAM && c.bias_correction) ? 1 : 0;
+  return b;
+}
+
 // Per-step scalars of update s in double, rounded once to fp32; launches
-// the clip-norm reduction first when the configuration clips.
-StepParams prepare_step(mtdao_handle* h, const void* grads, float lr, float adopt_clip, int64_t s, hipStream_t st) {
+// the clip-norm reduction first when the configuration clips.  With dev
+// the kernels take lr, the ADOPT clip and the bias-corrected weights from
+// the device-side step instead.
+StepParams prepare_step(mtdao_handle* h, const void* grads, float lr, float adopt_clip, int64_t s, hipStream_t st,
+                        const DeviceStep* dev = nullptr) {
   const mtdao_config& c = h->cfg;
   const int64_t P = c.numel;
   StepParams p;
@@ -630,19 +652,17 @@ StepParams prepare_step(mtdao_handle* h, const void* grads, float lr, float adop
   p.P = P;
   p.replicas = c.replicas;
   double wsum = 0.0;
-  const bool bc = c.form == MTDAO_ADAM && c.bias_correction;
   for (int j = 0; j < c.n_moments; ++j) {
-    const double b = c.beta1[j], w = c.omega[j];
     p.beta[j] = c.beta1[j];
-    p.omb[j] = (float)(1.0 - b);
-    p.w[j] = (float)(bc ? w / (1.0 - std::pow(b, (double)s)) : w);
-    wsum += w;
+    p.omb[j] = (float)(1.0 - (double)c.beta1[j]);
+    wsum += (double)c.omega[j];
   }
+  step_scalars(bias_correction_of(c), s, p.w, &p.inv_bc2);
   p.gw = (float)(1.0 - wsum);
   p.beta2 = c.beta2;
   p.omb2 = (float)(1.0 - (double)c.beta2);
-  p.inv_bc2 = (float)(bc ? 1.0 / (1.0 - std::pow((double)c.beta2, (double)s)) : 1.0);
   p.eps = c.eps;
+  p.dev = dev;
   p.lr = lr;
   p.clip = adopt_clip;
   p.scale = nullptr;
@@ -697,6 +717,41 @@ void launch_means(mtdao_handle* h, uint32_t m, bool outer_update, hipStream_t st
     xp.outer_state = outer_update ? 0 : -1;
     launch_mean<uint16_t>(xp, 1, vec_width(MTDAO_BF16, c.numel), st);
   }
+}
+
+// mtdao_step_sync after its argument checks; with dev, k_device_step first
+// advances the device-side step and fills its scalars, which the kernels
+// read instead of lr and adopt_clip.
+int32_t step_sync_launch(mtdao_handle* h, const void* grads, float lr, float adopt_clip, uint32_t mask,
+                         uint32_t* applied_mask, hipStream_t st, DeviceStep* dev, const float* lr_table,
+                         const float* clip_table, int64_t table_len) {
+  const int64_t s = h->s + 1;
+  uint32_t m;
+  int32_t r = resolve_mask(h, mask, s, &m);
+  if (r != MTDAO_OK) return r;
+  h->s = s;
+  if (applied_mask) *applied_mask = m;
+  const mtdao_config& c = h->cfg;
+  if (dev)
+    hipLaunchKernelGGL(k_device_step, dim3(1), dim3(64), 0, st, dev, bias_correction_of(c), lr_table, clip_table,
+                       table_len);
+  if (c.numel == 0) return dev ? hip_check(&h->err, hipGetLastError(), "mtdao_step_sync_device launch") : MTDAO_OK;
+  const StepParams p = prepare_step(h, grads, lr, adopt_clip, s, st, dev);
+  // s is new, so an outer step due here has not run yet
+  const bool outer_update = claim_outer_step(h, m, s);
+  // K = 1: the mean is the row; only an outer step on x still has work
+  const uint32_t work = c.replicas > 1 ? m : (outer_update ? 1u : 0u);
+  if (adopt_first_update(c, s)) {
+    launch_adopt_first(h, grads, st);
+    if (work != 0) launch_means(h, work, outer_update, st);
+  } else if (work == 0) {
+    launch_step(c, p, step_vec_width(c), st);
+  } else if (c.sync_order == MTDAO_SYNC_MOMENTA_IN_STEP && (work & ~1u) != 0) {
+    launch_sgdm_averaged_momenta(c, p, step_vec_width(c), work, st);
+  } else {
+    launch_step_sync(c, p, step_vec_width(c), work, st);
+  }
+  return hip_check(&h->err, hipGetLastError(), "mtdao_step_sync launch");
 }
 
 }  // namespace
@@ -890,31 +945,34 @@ int32_t mtdao_step_sync(mtdao_handle* h, const void* grads, float lr, float adop
   if (!h) return fail(&g_err, MTDAO_ERR_INVALID_ARG, "handle is NULL");
   int32_t r = check_step_args(h, grads, lr, adopt_clip);
   if (r != MTDAO_OK) return r;
-  const int64_t s = h->s + 1;
-  uint32_t m;
-  r = resolve_mask(h, mask, s, &m);
+  return step_sync_launch(h, grads, lr, adopt_clip, mask, applied_mask, reinterpret_cast<hipStream_t>(hip_stream),
+                          nullptr, nullptr, nullptr, 0);
+}
+
+int32_t mtdao_device_step_set(mtdao_handle* h, mtdao_device_step* d, int64_t s, void* hip_stream) {
+  if (!h) return fail(&g_err, MTDAO_ERR_INVALID_ARG, "handle is NULL");
+  if (!d) return fail(&h->err, MTDAO_ERR_INVALID_ARG, "device step is NULL");
+  if (!aligned16(d)) return fail(&h->err, MTDAO_ERR_ALIGN, "device step is not 16-byte aligned");
+  if (s < 0) return fail(&h->err, MTDAO_ERR_RANGE, "step %lld < 0", (long long)s);
+  hipLaunchKernelGGL(k_device_step_set, dim3(1), dim3(64), 0, reinterpret_cast<hipStream_t>(hip_stream),
+                     reinterpret_cast<DeviceStep*>(d), s);
+  return hip_check(&h->err, hipGetLastError(), "mtdao_device_step_set launch");
+}
+
+int32_t mtdao_step_sync_device(mtdao_handle* h, const void* grads, mtdao_device_step* d, const float* lr_table,
+                               const float* clip_table, int64_t table_len, uint32_t mask, uint32_t* applied_mask,
+                               void* hip_stream) {
+  if (!h) return fail(&g_err, MTDAO_ERR_INVALID_ARG, "handle is NULL");
+  int32_t r = check_step_args(h, grads, 0.0f, 0.0f);
   if (r != MTDAO_OK) return r;
-  h->s = s;
-  if (applied_mask) *applied_mask = m;
-  const mtdao_config& c = h->cfg;
-  if (c.numel == 0) return MTDAO_OK;
-  hipStream_t st = reinterpret_cast<hipStream_t>(hip_stream);
-  const StepParams p = prepare_step(h, grads, lr, adopt_clip, s, st);
-  // s is new, so an outer step due here has not run yet
-  const bool outer_update = claim_outer_step(h, m, s);
-  // K = 1: the mean is the row; only an outer step on x still has work
-  const uint32_t work = c.replicas > 1 ? m : (outer_update ? 1u : 0u);
-  if (adopt_first_update(c, s)) {
-    launch_adopt_first(h, grads, st);
-    if (work != 0) launch_means(h, work, outer_update, st);
-  } else if (work == 0) {
-    launch_step(c, p, step_vec_width(c), st);
-  } else if (c.sync_order == MTDAO_SYNC_MOMENTA_IN_STEP && (work & ~1u) != 0) {
-    launch_sgdm_averaged_momenta(c, p, step_vec_width(c), work, st);
-  } else {
-    launch_step_sync(c, p, step_vec_width(c), work, st);
-  }
-  return hip_check(&h->err, hipGetLastError(), "mtdao_step_sync launch");
+  if (!d || !lr_table) return fail(&h->err, MTDAO_ERR_INVALID_ARG, "device step or lr table is NULL");
+  if (!aligned16(d)) return fail(&h->err, MTDAO_ERR_ALIGN, "device step is not 16-byte aligned");
+  if (table_len < 1) return fail(&h->err, MTDAO_ERR_RANGE, "table_len %lld < 1", (long long)table_len);
+  if (adopt_first_update(h->cfg, h->s + 1))
+    return fail(&h->err, MTDAO_ERR_INVALID_ARG,
+                "ADOPT's first update (v = g^2 only) goes through mtdao_local_step or mtdao_step_sync");
+  return step_sync_launch(h, grads, 0.0f, 0.0f, mask, applied_mask, reinterpret_cast<hipStream_t>(hip_stream),
+                          reinterpret_cast<DeviceStep*>(d), lr_table, clip_table, table_len);
 }
 
 int32_t mtdao_read_state(mtdao_handle* h, int32_t state, int32_t replica, int64_t offset, int64_t count,

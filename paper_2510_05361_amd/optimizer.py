@@ -113,6 +113,28 @@ class MtdaoOptimizer:
         assert grads.is_contiguous() and grads.shape == (self.K, self.P)
         return abi.mtdao_step_sync(self.handle, grads.data_ptr(), lr, adopt_clip, mask, _stream())
 
+    def device_step(self, lr_table: torch.Tensor, clip_table: Optional[torch.Tensor] = None) -> None:
+        """Keep the update number on the device from now on (for HIP graph
+        capture): allocates the mtdao_device_step block on first use, sets
+        it to the current step count, and keeps the fp32 device tables of
+        eta_t (and c_t) indexed by s - 1 that step_sync_device reads (a
+        captured graph holds their addresses: keep them alive)."""
+        assert lr_table.dtype == torch.float32 and lr_table.is_contiguous() and lr_table.numel() >= 1
+        assert clip_table is None or (clip_table.dtype == torch.float32 and clip_table.numel() == lr_table.numel())
+        # one block for the optimizer's life: captured graphs keep its address
+        if getattr(self, "_dstep", None) is None:
+            self._dstep = torch.zeros(abi.MTDAO_DEVICE_STEP_BYTES // 4, dtype=torch.float32, device=self.x.device)
+        self._lr_table, self._clip_table = lr_table, clip_table
+        abi.mtdao_device_step_set(self.handle, self._dstep.data_ptr(), self.step_count, _stream())
+
+    def step_sync_device(self, grads: torch.Tensor, mask: int = abi.MTDAO_SYNC_AUTO) -> int:
+        """step_sync whose eta_t, c_t and bias corrections come from the
+        device-side update number (see device_step)."""
+        assert grads.is_contiguous() and grads.shape == (self.K, self.P)
+        clip = self._clip_table.data_ptr() if self._clip_table is not None else None
+        return abi.mtdao_step_sync_device(self.handle, grads.data_ptr(), self._dstep.data_ptr(),
+                                          self._lr_table.data_ptr(), clip, self._lr_table.numel(), mask, _stream())
+
     def sync(self, mask: int = abi.MTDAO_SYNC_AUTO) -> int:
         return abi.mtdao_sync(self.handle, mask, _stream())
 

@@ -328,14 +328,15 @@ def test_bf16_input_conversion():
 
 
 def test_binding_struct_layout_matches_header(tmp_path):
-    """Every field of mtdao_config and mtdao_buffers sits at the same offset
+    """Every field of mtdao_config, mtdao_buffers and mtdao_device_step sits at the same offset
     with the same size in the ctypes binding as in the C header (a stale
     mirror would hand the library garbage pointers)."""
     import ctypes
     import os
     import subprocess
 
-    structs = {"mtdao_config": abi.MtdaoConfig, "mtdao_buffers": abi.MtdaoBuffers}
+    structs = {"mtdao_config": abi.MtdaoConfig, "mtdao_buffers": abi.MtdaoBuffers,
+               "mtdao_device_step": abi.MtdaoDeviceStep}
     lines = ["#include <stdio.h>", "#include <stddef.h>", '#include "mtdao.h"', "int main(void) {"]
     for cname, py in structs.items():
         lines.append(f'  printf("{cname} sizeof %zu\\n", sizeof({cname}));')
@@ -402,5 +403,44 @@ def test_sync_stats_host_rules():
         with pytest.raises(abi.MtdaoError) as e:
             abi.mtdao_sync_stats_static(h, 1, None)
         assert e.value.code == abi.MTDAO_ERR_INVALID_ARG
+    finally:
+        abi.mtdao_destroy(h)
+
+
+def test_device_step_host_rules():
+    """mtdao_step_sync_device and mtdao_device_step_set reject bad arguments
+    before anything is enqueued (the step count does not move), and ADOPT's
+    first update (v only) must go through the host-scalar calls."""
+    cfg = good_cfg()
+    h = _fake_handle(cfg)
+    g = (1 << 44) + (1 << 40)
+    try:
+        with pytest.raises(abi.MtdaoError) as e:
+            abi.mtdao_device_step_set(h, None, 0, None)
+        assert e.value.code == abi.MTDAO_ERR_INVALID_ARG
+        with pytest.raises(abi.MtdaoError) as e:
+            abi.mtdao_device_step_set(h, (1 << 44) + 8, 0, None)
+        assert e.value.code == abi.MTDAO_ERR_ALIGN
+        with pytest.raises(abi.MtdaoError) as e:
+            abi.mtdao_device_step_set(h, 1 << 44, -1, None)
+        assert e.value.code == abi.MTDAO_ERR_RANGE
+        for d, lr, n, code in [(None, 1 << 45, 4, abi.MTDAO_ERR_INVALID_ARG), (1 << 44, None, 4, abi.MTDAO_ERR_INVALID_ARG),
+                               ((1 << 44) + 4, 1 << 45, 4, abi.MTDAO_ERR_ALIGN), (1 << 44, 1 << 45, 0, abi.MTDAO_ERR_RANGE)]:
+            with pytest.raises(abi.MtdaoError) as e:
+                abi.mtdao_step_sync_device(h, g, d, lr, None, n, abi.MTDAO_SYNC_AUTO, None)
+            assert e.value.code == code
+        with pytest.raises(abi.MtdaoError) as e:
+            abi.mtdao_step_sync_device(h, g, 1 << 44, 1 << 45, None, 4, 1 << 5, None)
+        assert e.value.code == abi.MTDAO_ERR_INVALID_ARG
+        assert abi.mtdao_step_count(h) == 0
+    finally:
+        abi.mtdao_destroy(h)
+    adopt = good_cfg(form="adopt", beta2=0.9999)
+    h = _fake_handle(adopt)
+    try:
+        with pytest.raises(abi.MtdaoError) as e:
+            abi.mtdao_step_sync_device(h, g, 1 << 44, 1 << 45, None, 4, abi.MTDAO_SYNC_AUTO, None)
+        assert e.value.code == abi.MTDAO_ERR_INVALID_ARG and "first update" in abi.mtdao_last_error(h)
+        assert abi.mtdao_step_count(h) == 0
     finally:
         abi.mtdao_destroy(h)

@@ -14,8 +14,15 @@ number of every period -- which is what these tests check, bit for bit,
 against eager calls on a second optimizer fed the same gradients, with
 eager work and a synchronisation between replays.  The handle's host step
 counter advances during capture, not on replay.
+
+With the update number kept on the device (mtdao_step_sync_device), the
+step-dependent scalars -- eta_t from a schedule table, ADOPT's c_t, Adam's
+bias corrections -- are formed on the device at every replay, so a window
+of Adam with bias correction or of ADOPT replays bit-identical to eager
+mtdao_step_sync calls given the same eta_t and c_t, replay after replay.
 """
 
+import numpy as np
 import pytest
 import torch
 
@@ -86,6 +93,71 @@ def test_graph_replay_equals_eager(case):
         for k, (a, b) in enumerate(zip(g_opt.states(), e_opt.states())):
             assert torch.equal(a, b), f"replay {r}: state {k} differs"
         log(f"  replay {r}: all {nst} states bit-identical to eager")
+    del graph
+    g_opt.close()
+    e_opt.close()
+
+
+DEVICE_CASES = {
+    # Adam with bias correction, periods 4 / 8 / 16: a window of 16 steps, K = 2 (fused means)
+    "adam_bias_corrected": (synth.small_variant(synth.WORKLOADS["adam_n2_k2_p1m"], 60_000, tail=40), 16),
+    # ADOPT, bf16 x and g, c_t from a table, K = 8, periods 2 / 4 / 4
+    "adopt_bf16_ct": (synth.small_variant(synth.WORKLOADS["adopt_n2_k8_p124m_bf16"], 30_000, tail=8)
+                      .replace(period_x=2, period_u=(4, 4), period_v=4), 4),
+    # clipped SGDM, K = 16 (wave-per-replica fused kernel), clip-norm pass inside the graph
+    "sgdm_clip_k16": (synth.small_variant(synth.WORKLOADS["sgdm_n2_k16_p354m_clip"], 40_000, tail=37)
+                      .replace(period_x=4, period_u=(2, 4)), 4),
+}
+
+
+@pytest.mark.parametrize("case", sorted(DEVICE_CASES))
+def test_graph_device_step_equals_eager(case):
+    w, window = DEVICE_CASES[case]
+    replays = 3
+    n_total = 1 + window * (replays + 1)
+    log(f"case graph device step {case} P={w.numel} K={w.replicas} window={window}")
+    d = torch.device("cuda:0")
+    dev = DeviceInputs(w, d)
+    cfg = abi.config_from_workload(w)
+    g_opt = MtdaoOptimizer(cfg, d, x0=dev.x0_row())
+    e_opt = MtdaoOptimizer(cfg, d, x0=dev.x0_row())
+    gdt = torch.bfloat16 if w.grad_dtype == "bf16" else torch.float32
+    grads = torch.empty((w.replicas, w.numel), dtype=gdt, device=d)
+    # a decaying eta_t schedule and ADOPT's c_t, indexed by s - 1
+    lr = np.array([w.lr * (1.0 - 0.5 * k / n_total) for k in range(n_total)], dtype=np.float32)
+    clip = np.array([w.adopt_clip_value(k + 1) for k in range(n_total)], dtype=np.float32)
+    lr_t, clip_t = torch.from_numpy(lr).to(d), torch.from_numpy(clip).to(d)
+    use_clip = w.form == "adopt"
+    # update 1 on the host path on both (ADOPT's first update sets v only)
+    dev.grads_into(1, grads)
+    g_opt.step_sync(grads, float(lr[0]), float(clip[0]))
+    e_opt.step_sync(grads, float(lr[0]), float(clip[0]))
+    g_opt.device_step(lr_t, clip_t if use_clip else None)
+    torch.cuda.synchronize()
+
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        captured = [g_opt.step_sync_device(grads) for _ in range(window)]
+    torch.cuda.synchronize()
+    ocfg = oracle.OracleConfig.from_workload(w)
+    assert captured == [oracle.schedule(ocfg, s) for s in range(2, window + 2)]
+    s = 1
+    for r in range(replays):
+        dev.grads_into(r + 2, grads)  # eager work between replays
+        torch.cuda.synchronize()
+        graph.replay()
+        for _ in range(window):
+            s += 1
+            e_opt.step_sync(grads, float(lr[s - 1]), float(clip[s - 1]) if use_clip else 0.0)
+        torch.cuda.synchronize()
+        for k, (a, b) in enumerate(zip(g_opt.states(), e_opt.states())):
+            assert torch.equal(a, b), f"replay {r}: state {k} differs"
+        step = abi.MtdaoDeviceStep()
+        blob = g_opt._dstep.cpu().numpy().tobytes()
+        import ctypes
+        ctypes.memmove(ctypes.addressof(step), blob, ctypes.sizeof(step))
+        assert step.s == s and step.lr == lr[s - 1]
+        log(f"  replay {r}: steps up to {s}, every state bit-identical to eager")
     del graph
     g_opt.close()
     e_opt.close()
