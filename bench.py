@@ -485,6 +485,7 @@ def measure_graph(args) -> int:
     def eager_device():
         for _ in range(window):
             opt.step_sync_device(opt.grad)
+        opt.device_step_advance()
 
     for _ in range(args.warmup):
         eager()

@@ -234,43 +234,45 @@ int32_t mtdao_sync(mtdao_handle* h, uint32_t mask, uint32_t* applied_mask, void*
 int32_t mtdao_step_sync(mtdao_handle* h, const void* grads, float lr, float adopt_clip, uint32_t mask,
                         uint32_t* applied_mask, void* hip_stream);
 
-/* The update number kept in device memory, for capture into a HIP graph:
- * a replayed window of mtdao_step_sync_device calls computes the
+/* The update count kept in device memory, for capture into a HIP graph:
+ * a replayed window of mtdao_step_sync_device calls forms the
  * step-dependent scalars of every update (eta_t, c_t, Adam's bias
- * corrections) from the device-side s instead of the values frozen at
- * capture.  Caller-owned device memory, 16-byte aligned; the kernels write
- * every field but s from s. */
+ * corrections) from the device-side count instead of values frozen at
+ * capture.  Caller-owned device memory, 16-byte aligned. */
 typedef struct mtdao_device_step {
-  int64_t s;                /* updates applied                                       */
-  float lr;                 /* eta_t of update s                                     */
-  float adopt_clip;         /* c_t of update s (<= 0: off)                           */
-  float w[MTDAO_MAX_N];     /* omega_j, over (1 - beta_{1,j}^s) under bias correction */
-  float inv_bc2;            /* 1 / (1 - beta_2^s) under bias correction, else 1      */
-  float reserved;
+  int64_t s;                /* update count as of the last set or advance */
+  int64_t reserved;
 } mtdao_device_step;
 
-/* Enqueue d->s = s (e.g. mtdao_step_count at set-up).  Nothing else is
- * touched; no memset is recorded. */
+/* Enqueue d->s = s; the host side records the handle's current step count
+ * as the base of later offsets (typically s = mtdao_step_count).  No memset
+ * is recorded. */
 int32_t mtdao_device_step_set(mtdao_handle* h, mtdao_device_step* d, int64_t s, void* hip_stream);
 
-/* mtdao_step_sync whose update number lives in d: it enqueues the advance
- * d->s += 1 and the scalars of update s = d->s (eta_t = lr_table[s - 1],
- * c_t = clip_table[s - 1] or off when clip_table is NULL; the last entry
- * for s > table_len; the bias corrections of Algorithm 1 with this s),
- * then the same kernels as mtdao_step_sync, which read those scalars on
- * the device.  The tables are caller-owned device fp32 arrays.  Results
- * equal mtdao_step_sync's with the same eta_t and c_t, bit for bit (the
- * scalars are formed by the same code on host and device).  The mask
- * (MTDAO_SYNC_AUTO: the schedule at the handle's host step count + 1) and
- * the launch configuration are taken at call time: a captured window
- * replays the masks of the captured steps, so it equals eager calls when it
- * spans a whole number of every period.  The handle's host step count
- * advances per call as in mtdao_step_sync; on replay only d->s advances.
- * ADOPT's first update (previous-v order, s = 1) is rejected here: it sets
- * v only, through mtdao_local_step or mtdao_step_sync. */
+/* mtdao_step_sync whose update number is taken on the device: the k-th
+ * call since the last set or advance performs update s = d->s + k, with
+ * eta_t = lr_table[s - 1] and c_t = clip_table[s - 1] (or off when
+ * clip_table is NULL; the last entries for s > table_len) and the bias
+ * corrections of Algorithm 1 formed from this s by the kernels.  The
+ * tables are caller-owned device fp32 arrays.  Results equal
+ * mtdao_step_sync's with the same eta_t and c_t, bit for bit (the scalars
+ * are formed by the same code on host and device).  k, the mask
+ * (MTDAO_SYNC_AUTO: the schedule at the handle's step count + 1) and the
+ * launch configuration are fixed at call time: a captured window replays
+ * the masks of the captured steps, so it equals eager calls when it spans
+ * a whole number of every period.  The handle's host step count advances
+ * per call as in mtdao_step_sync.  ADOPT's first update (previous-v order,
+ * s = 1) is rejected: it sets v only, through mtdao_local_step or
+ * mtdao_step_sync. */
 int32_t mtdao_step_sync_device(mtdao_handle* h, const void* grads, mtdao_device_step* d, const float* lr_table,
                                const float* clip_table, int64_t table_len, uint32_t mask, uint32_t* applied_mask,
                                void* hip_stream);
+
+/* Enqueue d->s += n, n = the mtdao_step_sync_device calls since the last
+ * set or advance (fixed at call time, so a window captured with its
+ * advance moves d->s on by the window at every replay); nothing when
+ * n = 0. */
+int32_t mtdao_device_step_advance(mtdao_handle* h, mtdao_device_step* d, void* hip_stream);
 
 /* Device scratch (bytes) that mtdao_sync_stats needs for this
  * configuration: the 3 + 2K fp64 sums of every workgroup of the

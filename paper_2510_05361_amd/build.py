@@ -30,9 +30,9 @@ FLAGS = [
 ]
 
 
-def _compile(src: str, out: str, extra=()) -> str:
+def _compile(src: str, out: str, extra=(), libs=()) -> str:
     tmp = out + ".tmp"
-    cmd = [HIPCC, *FLAGS, *extra, "-I", os.path.join(ROOT, "include"), "-o", tmp, src]
+    cmd = [HIPCC, *FLAGS, *extra, "-I", os.path.join(ROOT, "include"), "-o", tmp, src, *libs]
     subprocess.run(cmd, check=True)
     os.replace(tmp, out)
     return out
@@ -42,7 +42,8 @@ def build(out: str = LIB, extra=()) -> str:
     """The optimizer library (always) and the benchmark's stream-reference
     kernels (libstream_ref.so)."""
     _compile(STREAM_SRC, STREAM_LIB, extra)
-    return _compile(SRC, out, extra)
+    # roctx ranges (MTDAO_ROCTX=1) come from the rocprofiler-sdk marker library
+    return _compile(SRC, out, extra, libs=("-L/opt/rocm/lib", "-lrocprofiler-sdk-roctx", "-Wl,-rpath,/opt/rocm/lib"))
 
 
 if __name__ == "__main__":

@@ -222,16 +222,12 @@ __device__ __forceinline__ void outer_step_piece(const OuterParams& o, int64_t e
 
 enum StepWindows { kWinOne = 0, kWinHalves = 1, kWinPairs = 2 };
 
-// Step-dependent scalars of update s, for launches whose update number is
-// kept on the device (graph replay): k_device_step advances s and fills the
-// rest.  The layout is mtdao_device_step of the C header.
+// The update count kept on the device for graph replay (the layout of
+// mtdao_device_step): a launch at offset k after the last advance takes
+// update s = s + k; k_device_step_add moves s on by a window of calls.
 struct DeviceStep {
-  int64_t s;           // updates applied
-  float lr;            // eta_t of update s
-  float clip;          // ADOPT c_t of update s (<= 0: no clamp)
-  float w[kMaxN];      // omega_j, times 1/(1 - beta_{1,j}^s) under bias correction
-  float inv_bc2;       // 1/(1 - beta_2^s) under bias correction, else 1
-  float reserved;
+  int64_t s;
+  int64_t reserved;
 };
 
 // b^s for s >= 0 by repeated squaring in plain IEEE double multiplies, so
@@ -258,7 +254,7 @@ struct BiasCorrection {
 
 // w_j = omega_j / (1 - beta_j^s) and 1 / (1 - beta_2^s) (omega_j and 1
 // without correction) in double, rounded once to fp32; the same code on
-// the host (eager calls) and in k_device_step (device-side s).
+// the host (eager calls) and in the kernels (device-side s).
 __host__ __device__ inline void step_scalars(const BiasCorrection& c, int64_t s, float* w, float* inv_bc2) {
 #pragma clang fp contract(off)
   for (int j = 0; j < c.n; ++j)
@@ -266,27 +262,12 @@ __host__ __device__ inline void step_scalars(const BiasCorrection& c, int64_t s,
   *inv_bc2 = (float)(c.on ? 1.0 / (1.0 - pow_steps((double)c.beta2, s)) : 1.0);
 }
 
-// One thread: s += 1, then the scalars of update s; eta_t and c_t from
-// tables indexed by s - 1 (the last entry for s beyond the table).
-__global__ __launch_bounds__(64) void k_device_step(DeviceStep* __restrict__ d, BiasCorrection c,
-                                                   const float* __restrict__ lr_table,
-                                                   const float* __restrict__ clip_table, int64_t len) {
-  if (threadIdx.x != 0) return;
-  const int64_t s = d->s + 1;
-  const int64_t i = (s < len ? s : len) - 1;
-  float w[kMaxN] = {0.0f, 0.0f, 0.0f, 0.0f}, ib;
-  step_scalars(c, s, w, &ib);
-  d->s = s;
-  d->lr = lr_table[i];
-  d->clip = clip_table != nullptr ? clip_table[i] : 0.0f;
-#pragma unroll
-  for (int j = 0; j < kMaxN; ++j) d->w[j] = w[j];
-  d->inv_bc2 = ib;
-}
-
-// d->s = s (the other fields are filled by the next k_device_step).
 __global__ __launch_bounds__(64) void k_device_step_set(DeviceStep* __restrict__ d, int64_t s) {
   if (threadIdx.x == 0) d->s = s;
+}
+
+__global__ __launch_bounds__(64) void k_device_step_add(DeviceStep* __restrict__ d, int64_t n) {
+  if (threadIdx.x == 0) d->s = d->s + n;
 }
 
 // Per-launch scalars, prepared on the host in double and rounded to fp32.
@@ -310,19 +291,37 @@ struct StepParams {
   float lr;                // eta_t
   float clip;              // ADOPT c_t (<= 0: no clamp)
   OuterParams outer;       // OuterOpt applied when x is averaged
-  const DeviceStep* dev;   // non-null: lr, clip, w and inv_bc2 are read from it
+  // device-side update number (graph replay): when dev is non-null the
+  // update is s = dev->s + dev_k, and lr, clip, w and inv_bc2 are formed
+  // from it: eta_t = lr_table[s - 1], c_t = clip_table[s - 1] (the last
+  // entries beyond table_len; clip off without a table), corrections from bc
+  const DeviceStep* dev;
+  int64_t dev_k;
+  const float* lr_table;
+  const float* clip_table;
+  int64_t table_len;
+  BiasCorrection bc;
 };
 
 // The launch's scalars: those of the argument block, or those of the
-// device-side step when it is given.
+// device-side update number when it is given (every workgroup forms them;
+// a few dozen double multiplies).
 __device__ __forceinline__ StepParams device_scalars(const StepParams& p0) {
+#pragma clang fp contract(off)
   if (p0.dev == nullptr) return p0;
   StepParams p = p0;
-  p.lr = p0.dev->lr;
-  p.clip = p0.dev->clip;
-  p.inv_bc2 = p0.dev->inv_bc2;
+  const int64_t s = p0.dev->s + p0.dev_k;
+  const int64_t i = (s < p0.table_len ? s : p0.table_len) - 1;
+  p.lr = p0.lr_table[i];
+  p.clip = p0.clip_table != nullptr ? p0.clip_table[i] : 0.0f;
+  // step_scalars with the moment loop unrolled (a runtime-indexed store
+  // would put the whole parameter block in private memory)
 #pragma unroll
-  for (int j = 0; j < kMaxN; ++j) p.w[j] = p0.dev->w[j];
+  for (int j = 0; j < kMaxN; ++j)
+    if (j < p0.bc.n)
+      p.w[j] = (float)(p0.bc.on ? (double)p0.bc.omega[j] / (1.0 - pow_steps((double)p0.bc.beta[j], s))
+                                : (double)p0.bc.omega[j]);
+  p.inv_bc2 = (float)(p0.bc.on ? 1.0 / (1.0 - pow_steps((double)p0.bc.beta2, s)) : 1.0);
   return p;
 }
 
@@ -397,29 +396,28 @@ __device__ __forceinline__ void update_element(const StepParams& p, float sc, fl
 template <int FORM, int N, typename XT, typename GT, int V, int U, int NTM, int ORDER, int B = kBlock, int C = 0,
           int WIN = kWinOne>
 __global__ __launch_bounds__(B) void k_local_step(StepParams p0) {
-  const StepParams p = device_scalars(p0);
   constexpr bool NTL = (NTM & 1) != 0, NTS = (NTM & 2) != 0;
 
-  for (int64_t tile = blockIdx.x; tile < p.tiles; tile += gridDim.x) {
+  for (int64_t tile = blockIdx.x; tile < p0.tiles; tile += gridDim.x) {
     // the row m and the range [base, end) of it that this tile belongs to
     const int64_t w = WIN == kWinOne ? 0 : (tile & 1);
     const int64_t wt = WIN == kWinOne ? tile : (tile >> 1);
-    int64_t m = blockIdx.y, base = 0, end = p.P;
+    int64_t m = blockIdx.y, base = 0, end = p0.P;
     if constexpr (WIN == kWinHalves) {
-      base = w * p.wlen;
-      end = w == 0 ? p.wlen : p.P;
+      base = w * p0.wlen;
+      end = w == 0 ? p0.wlen : p0.P;
     } else if constexpr (WIN == kWinPairs) {
       m += w * (int64_t)gridDim.y;
-      if (m >= p.replicas) continue;  // odd K: the last row has no partner
+      if (m >= p0.replicas) continue;  // odd K: the last row has no partner
     }
-    const int64_t row = m * p.P;
-    XT* __restrict__ x = reinterpret_cast<XT*>(p.x) + row;
-    const GT* __restrict__ g = reinterpret_cast<const GT*>(p.g) + row;
+    const int64_t row = m * p0.P;
+    XT* __restrict__ x = reinterpret_cast<XT*>(p0.x) + row;
+    const GT* __restrict__ g = reinterpret_cast<const GT*>(p0.g) + row;
     float* __restrict__ u[N];
 #pragma unroll
-    for (int j = 0; j < N; ++j) u[j] = p.u[j] + row;
-    float* __restrict__ v = (FORM == kSgdm) ? nullptr : p.v + row;
-    const float sc = (FORM != kAdopt && p.scale != nullptr) ? p.scale[m] : 1.0f;
+    for (int j = 0; j < N; ++j) u[j] = p0.u[j] + row;
+    float* __restrict__ v = (FORM == kSgdm) ? nullptr : p0.v + row;
+    const float sc = (FORM != kAdopt && p0.scale != nullptr) ? p0.scale[m] : 1.0f;
     float gv[U][V], xv[U][V], uv[U][N][V], vv[U][V];
     // issue every load of the tile before any arithmetic
 #pragma unroll
@@ -433,6 +431,9 @@ __global__ __launch_bounds__(B) void k_local_step(StepParams p0) {
         if constexpr (FORM != kSgdm) load_v<float, V, NTL>(v, e, vv[k]);
       }
     }
+    // the step-dependent scalars after the loads are in flight (from the
+    // device-side update number when there is one)
+    const StepParams p = device_scalars(p0);
 #pragma unroll
     for (int k = 0; k < U; ++k) {
       const int64_t e = base + tile_elem<B * V * U, C>(wt, (k * B + (int)threadIdx.x) * V);
@@ -603,28 +604,29 @@ constexpr int kWaveMaxK = 16;
 template <int FORM, int N, typename XT, typename GT, int V, int NTM, int ORDER>
 __global__ __launch_bounds__(64 * kWaveMaxK) __attribute__((amdgpu_waves_per_eu(8)))
 void k_local_step_sync_waves(StepParams p0, uint32_t mask, int32_t K) {
-  const StepParams p = device_scalars(p0);
   constexpr bool NTL = (NTM & 1) != 0, NTS = (NTM & 2) != 0;
   constexpr int NS = 2 + N;  // x, u^1..u^N, v
   __shared__ float lds[kWaveMaxK][64 * V];
   const int32_t m = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  XT* __restrict__ x = reinterpret_cast<XT*>(p.x);
-  const GT* __restrict__ g = reinterpret_cast<const GT*>(p.g);
+  XT* __restrict__ x = reinterpret_cast<XT*>(p0.x);
+  const GT* __restrict__ g = reinterpret_cast<const GT*>(p0.g);
   const double rk = 1.0 / (double)K;
-  const float sc = (FORM != kAdopt && p.scale != nullptr) ? p.scale[m] : 1.0f;
+  const float sc = (FORM != kAdopt && p0.scale != nullptr) ? p0.scale[m] : 1.0f;
 
-  for (int64_t tile = blockIdx.x; tile < p.tiles; tile += gridDim.x) {
+  for (int64_t tile = blockIdx.x; tile < p0.tiles; tile += gridDim.x) {
     const int64_t e = tile * (int64_t)(64 * V) + (int64_t)lane * V;
-    const bool in = e < p.P;
-    const int64_t r = (int64_t)m * p.P + e;
+    const bool in = e < p0.P;
+    const int64_t r = (int64_t)m * p0.P + e;
     float val[NS][V];  // updated x, u^j, v of this lane's elements
     if (in) {
       float gv[V], uv[N][V];
       load_v<GT, V, NTL>(g, r, gv);
       load_v<XT, V, NTL>(x, r, val[0]);
 #pragma unroll
-      for (int j = 0; j < N; ++j) load_v<float, V, NTL>(p.u[j], r, uv[j]);
-      if constexpr (FORM != kSgdm) load_v<float, V, NTL>(p.v, r, val[NS - 1]);
+      for (int j = 0; j < N; ++j) load_v<float, V, NTL>(p0.u[j], r, uv[j]);
+      if constexpr (FORM != kSgdm) load_v<float, V, NTL>(p0.v, r, val[NS - 1]);
+      // the step-dependent scalars after the loads are in flight
+      const StepParams p = device_scalars(p0);
 #pragma unroll
       for (int t = 0; t < V; ++t) {
         float uu[N];
@@ -645,8 +647,8 @@ void k_local_step_sync_waves(StepParams p0, uint32_t mask, int32_t K) {
       if (!due) {
         if (!in) continue;
         if (k == 0) store_v<XT, V, NTS>(x, r, val[0]);
-        else if (k == NS - 1) store_v<float, V, NTS>(p.v, r, val[k]);
-        else store_v<float, V, NTS>(p.u[k - 1], r, val[k]);
+        else if (k == NS - 1) store_v<float, V, NTS>(p0.v, r, val[k]);
+        else store_v<float, V, NTS>(p0.u[k - 1], r, val[k]);
         continue;
       }
 #pragma unroll
@@ -661,8 +663,8 @@ void k_local_step_sync_waves(StepParams p0, uint32_t mask, int32_t K) {
         lds[0][t * 64 + lane] = mean_of(s0, d, rk);
       }
       __syncthreads();
-      if (k == 0 && p.outer.xo != nullptr) {
-        outer_step_piece<V>(p.outer, tile * (int64_t)(64 * V), p.P, K, m, lane, &lds[0][0]);
+      if (k == 0 && p0.outer.xo != nullptr) {
+        outer_step_piece<V>(p0.outer, tile * (int64_t)(64 * V), p0.P, K, m, lane, &lds[0][0]);
         __syncthreads();
       }
       if (in) {
@@ -670,8 +672,8 @@ void k_local_step_sync_waves(StepParams p0, uint32_t mask, int32_t K) {
 #pragma unroll
         for (int t = 0; t < V; ++t) mean[t] = lds[0][t * 64 + lane];
         if (k == 0) store_v<XT, V, NTS>(x, r, mean);
-        else if (k == NS - 1) store_v<float, V, NTS>(p.v, r, mean);
-        else store_v<float, V, NTS>(p.u[k - 1], r, mean);
+        else if (k == NS - 1) store_v<float, V, NTS>(p0.v, r, mean);
+        else store_v<float, V, NTS>(p0.u[k - 1], r, mean);
       }
       __syncthreads();
     }

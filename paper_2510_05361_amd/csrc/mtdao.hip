@@ -3,12 +3,14 @@
 // The arithmetic of every step runs in the kernels of kernels.hpp.
 
 #include <hip/hip_runtime.h>
+#include <rocprofiler-sdk-roctx/roctx.h>
 
 #include <algorithm>
 #include <cmath>
 #include <cstdarg>
 #include <cstddef>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <mutex>
 #include <string>
@@ -20,9 +22,7 @@
 
 using namespace mtdao;
 
-static_assert(sizeof(DeviceStep) == sizeof(mtdao_device_step) && offsetof(DeviceStep, lr) == offsetof(mtdao_device_step, lr) &&
-                  offsetof(DeviceStep, w) == offsetof(mtdao_device_step, w) &&
-                  offsetof(DeviceStep, inv_bc2) == offsetof(mtdao_device_step, inv_bc2),
+static_assert(sizeof(DeviceStep) == sizeof(mtdao_device_step) && offsetof(DeviceStep, s) == offsetof(mtdao_device_step, s),
               "DeviceStep mirrors mtdao_device_step");
 
 struct mtdao_handle {
@@ -38,12 +38,39 @@ struct mtdao_handle {
   int32_t norm_blocks = 0;
   int64_t s = 0;                    // local updates applied
   int64_t outer_done_s = -1;        // Nesterov: step s whose outer step has run
+  int64_t dev_base = 0;             // host count at the last device-step set or advance
   std::string err;
 };
 
 namespace {
 
 thread_local std::string g_err;
+
+// roctx ranges around every enqueueing call, for timelines of
+// rocprofv3 --marker-trace: on when MTDAO_ROCTX=1 in the environment.
+bool roctx_on() {
+  static const bool on = [] {
+    const char* e = std::getenv("MTDAO_ROCTX");
+    return e != nullptr && e[0] == '1';
+  }();
+  return on;
+}
+
+struct RoctxRange {
+  bool on;
+  explicit RoctxRange(const char* fmt, ...) : on(roctx_on()) {
+    if (!on) return;
+    char buf[128];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    roctxRangePushA(buf);
+  }
+  ~RoctxRange() {
+    if (on) roctxRangePop();
+  }
+};
 
 // Vector slots per thread in the local step: one for every form (measured
 // on MI355X with 1 KiB pieces: two slots were 0-0.5 % slower for Adam's
@@ -635,12 +662,21 @@ BiasCorrection bias_correction_of(const mtdao_config& c) {
   return b;
 }
 
+// Where a launch takes its update number from on the device.
+struct DeviceSource {
+  const DeviceStep* dev = nullptr;
+  int64_t k = 0;
+  const float* lr_table = nullptr;
+  const float* clip_table = nullptr;
+  int64_t len = 0;
+};
+
 // Per-step scalars of update s in double, rounded once to fp32; launches
-// the clip-norm reduction first when the configuration clips.  With dev
-// the kernels take lr, the ADOPT clip and the bias-corrected weights from
-// the device-side step instead.
+// the clip-norm reduction first when the configuration clips.  With a
+// device source the kernels form lr, the ADOPT clip and the bias-corrected
+// weights from the device-side update number instead.
 StepParams prepare_step(mtdao_handle* h, const void* grads, float lr, float adopt_clip, int64_t s, hipStream_t st,
-                        const DeviceStep* dev = nullptr) {
+                        const DeviceSource& ds = DeviceSource()) {
   const mtdao_config& c = h->cfg;
   const int64_t P = c.numel;
   StepParams p;
@@ -662,7 +698,12 @@ StepParams prepare_step(mtdao_handle* h, const void* grads, float lr, float adop
   p.beta2 = c.beta2;
   p.omb2 = (float)(1.0 - (double)c.beta2);
   p.eps = c.eps;
-  p.dev = dev;
+  p.dev = ds.dev;
+  p.dev_k = ds.k;
+  p.lr_table = ds.lr_table;
+  p.clip_table = ds.clip_table;
+  p.table_len = ds.len;
+  p.bc = bias_correction_of(c);
   p.lr = lr;
   p.clip = adopt_clip;
   p.scale = nullptr;
@@ -719,24 +760,21 @@ void launch_means(mtdao_handle* h, uint32_t m, bool outer_update, hipStream_t st
   }
 }
 
-// mtdao_step_sync after its argument checks; with dev, k_device_step first
-// advances the device-side step and fills its scalars, which the kernels
-// read instead of lr and adopt_clip.
+// mtdao_step_sync after its argument checks; with a device source the
+// kernels form their step-dependent scalars from the device-side update
+// number.
 int32_t step_sync_launch(mtdao_handle* h, const void* grads, float lr, float adopt_clip, uint32_t mask,
-                         uint32_t* applied_mask, hipStream_t st, DeviceStep* dev, const float* lr_table,
-                         const float* clip_table, int64_t table_len) {
+                         uint32_t* applied_mask, hipStream_t st, const DeviceSource& ds) {
   const int64_t s = h->s + 1;
+  const RoctxRange range("%s s=%lld mask=0x%x", ds.dev ? "mtdao_step_sync_device" : "mtdao_step_sync", (long long)s, mask);
   uint32_t m;
   int32_t r = resolve_mask(h, mask, s, &m);
   if (r != MTDAO_OK) return r;
   h->s = s;
   if (applied_mask) *applied_mask = m;
   const mtdao_config& c = h->cfg;
-  if (dev)
-    hipLaunchKernelGGL(k_device_step, dim3(1), dim3(64), 0, st, dev, bias_correction_of(c), lr_table, clip_table,
-                       table_len);
-  if (c.numel == 0) return dev ? hip_check(&h->err, hipGetLastError(), "mtdao_step_sync_device launch") : MTDAO_OK;
-  const StepParams p = prepare_step(h, grads, lr, adopt_clip, s, st, dev);
+  if (c.numel == 0) return MTDAO_OK;
+  const StepParams p = prepare_step(h, grads, lr, adopt_clip, s, st, ds);
   // s is new, so an outer step due here has not run yet
   const bool outer_update = claim_outer_step(h, m, s);
   // K = 1: the mean is the row; only an outer step on x still has work
@@ -760,6 +798,7 @@ extern "C" {
 
 int32_t mtdao_local_step(mtdao_handle* h, const void* grads, float lr, float adopt_clip, void* hip_stream) {
   if (!h) return fail(&g_err, MTDAO_ERR_INVALID_ARG, "handle is NULL");
+  const RoctxRange range("mtdao_local_step s=%lld", (long long)(h->s + 1));
   int32_t r = check_step_args(h, grads, lr, adopt_clip);
   if (r != MTDAO_OK) return r;
   const int64_t s = ++h->s;
@@ -773,6 +812,7 @@ int32_t mtdao_local_step(mtdao_handle* h, const void* grads, float lr, float ado
 
 int32_t mtdao_sync(mtdao_handle* h, uint32_t mask, uint32_t* applied_mask, void* hip_stream) {
   if (!h) return fail(&g_err, MTDAO_ERR_INVALID_ARG, "handle is NULL");
+  const RoctxRange range("mtdao_sync s=%lld mask=0x%x", (long long)h->s, mask);
   uint32_t m;
   int32_t r = resolve_mask(h, mask, h->s, &m);
   if (r != MTDAO_OK) return r;
@@ -841,6 +881,7 @@ int32_t check_stats_args(mtdao_handle* h, double* host_stats) {
 // finalized rows copied to host_stats through a buffer on the stack.
 int32_t run_sync_stats(mtdao_handle* h, uint32_t mask, uint32_t* applied_mask, double* scratch, double* host_stats,
                        hipStream_t st) {
+  const RoctxRange range("mtdao_sync_stats s=%lld mask=0x%x", (long long)h->s, mask);
   const mtdao_config& c = h->cfg;
   uint32_t m;
   int32_t r = resolve_mask(h, mask, h->s, &m);
@@ -946,7 +987,7 @@ int32_t mtdao_step_sync(mtdao_handle* h, const void* grads, float lr, float adop
   int32_t r = check_step_args(h, grads, lr, adopt_clip);
   if (r != MTDAO_OK) return r;
   return step_sync_launch(h, grads, lr, adopt_clip, mask, applied_mask, reinterpret_cast<hipStream_t>(hip_stream),
-                          nullptr, nullptr, nullptr, 0);
+                          DeviceSource());
 }
 
 int32_t mtdao_device_step_set(mtdao_handle* h, mtdao_device_step* d, int64_t s, void* hip_stream) {
@@ -954,9 +995,25 @@ int32_t mtdao_device_step_set(mtdao_handle* h, mtdao_device_step* d, int64_t s, 
   if (!d) return fail(&h->err, MTDAO_ERR_INVALID_ARG, "device step is NULL");
   if (!aligned16(d)) return fail(&h->err, MTDAO_ERR_ALIGN, "device step is not 16-byte aligned");
   if (s < 0) return fail(&h->err, MTDAO_ERR_RANGE, "step %lld < 0", (long long)s);
+  int32_t r;
   hipLaunchKernelGGL(k_device_step_set, dim3(1), dim3(64), 0, reinterpret_cast<hipStream_t>(hip_stream),
                      reinterpret_cast<DeviceStep*>(d), s);
-  return hip_check(&h->err, hipGetLastError(), "mtdao_device_step_set launch");
+  r = hip_check(&h->err, hipGetLastError(), "mtdao_device_step_set launch");
+  if (r == MTDAO_OK) h->dev_base = h->s;
+  return r;
+}
+
+int32_t mtdao_device_step_advance(mtdao_handle* h, mtdao_device_step* d, void* hip_stream) {
+  if (!h) return fail(&g_err, MTDAO_ERR_INVALID_ARG, "handle is NULL");
+  if (!d) return fail(&h->err, MTDAO_ERR_INVALID_ARG, "device step is NULL");
+  if (!aligned16(d)) return fail(&h->err, MTDAO_ERR_ALIGN, "device step is not 16-byte aligned");
+  const int64_t n = h->s - h->dev_base;
+  if (n == 0) return MTDAO_OK;
+  hipLaunchKernelGGL(k_device_step_add, dim3(1), dim3(64), 0, reinterpret_cast<hipStream_t>(hip_stream),
+                     reinterpret_cast<DeviceStep*>(d), n);
+  const int32_t r = hip_check(&h->err, hipGetLastError(), "mtdao_device_step_advance launch");
+  if (r == MTDAO_OK) h->dev_base = h->s;
+  return r;
 }
 
 int32_t mtdao_step_sync_device(mtdao_handle* h, const void* grads, mtdao_device_step* d, const float* lr_table,
@@ -971,8 +1028,13 @@ int32_t mtdao_step_sync_device(mtdao_handle* h, const void* grads, mtdao_device_
   if (adopt_first_update(h->cfg, h->s + 1))
     return fail(&h->err, MTDAO_ERR_INVALID_ARG,
                 "ADOPT's first update (v = g^2 only) goes through mtdao_local_step or mtdao_step_sync");
-  return step_sync_launch(h, grads, 0.0f, 0.0f, mask, applied_mask, reinterpret_cast<hipStream_t>(hip_stream),
-                          reinterpret_cast<DeviceStep*>(d), lr_table, clip_table, table_len);
+  DeviceSource ds;
+  ds.dev = reinterpret_cast<const DeviceStep*>(d);
+  ds.k = h->s + 1 - h->dev_base;
+  ds.lr_table = lr_table;
+  ds.clip_table = clip_table;
+  ds.len = table_len;
+  return step_sync_launch(h, grads, 0.0f, 0.0f, mask, applied_mask, reinterpret_cast<hipStream_t>(hip_stream), ds);
 }
 
 int32_t mtdao_read_state(mtdao_handle* h, int32_t state, int32_t replica, int64_t offset, int64_t count,

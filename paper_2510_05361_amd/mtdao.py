@@ -102,6 +102,8 @@ def lib() -> ctypes.CDLL:
         L.mtdao_device_step_set.restype = I32
         L.mtdao_step_sync_device.argtypes = [VP, VP, VP, VP, VP, I64, U32, P(U32), VP]
         L.mtdao_step_sync_device.restype = I32
+        L.mtdao_device_step_advance.argtypes = [VP, VP, VP]
+        L.mtdao_device_step_advance.restype = I32
         L.mtdao_schedule.argtypes = [P(MtdaoConfig), I64, P(U32)]
         L.mtdao_schedule.restype = I32
         L.mtdao_read_state.argtypes = [VP, I32, I32, I64, I64, VP, VP]
@@ -257,8 +259,7 @@ def mtdao_sync_stats_static(h: int, mask: int, stream: Optional[int]):
 
 class MtdaoDeviceStep(ctypes.Structure):
     """Layout of mtdao_device_step (the block lives in device memory)."""
-    _fields_ = [("s", ctypes.c_int64), ("lr", ctypes.c_float), ("adopt_clip", ctypes.c_float),
-                ("w", ctypes.c_float * MTDAO_MAX_N), ("inv_bc2", ctypes.c_float), ("reserved", ctypes.c_float)]
+    _fields_ = [("s", ctypes.c_int64), ("reserved", ctypes.c_int64)]
 
 
 MTDAO_DEVICE_STEP_BYTES = ctypes.sizeof(MtdaoDeviceStep)
@@ -270,13 +271,17 @@ def mtdao_device_step_set(h: int, d: int, s: int, stream: Optional[int]) -> None
 
 def mtdao_step_sync_device(h: int, grads: int, d: int, lr_table: int, clip_table: Optional[int], table_len: int,
                            mask: int, stream: Optional[int]) -> int:
-    """mtdao_step_sync with the update number and its scalars on the
-    device (d: mtdao_device_step, tables: device fp32 arrays); returns the
-    applied mask."""
+    """mtdao_step_sync with the update number taken on the device (d:
+    mtdao_device_step, tables: device fp32 arrays); returns the applied
+    mask."""
     applied = ctypes.c_uint32(0)
     _check(lib().mtdao_step_sync_device(h, grads, d, lr_table, clip_table, int(table_len), int(mask) & 0xFFFFFFFF,
                                         ctypes.byref(applied), stream), h)
     return int(applied.value)
+
+
+def mtdao_device_step_advance(h: int, d: int, stream: Optional[int]) -> None:
+    _check(lib().mtdao_device_step_advance(h, d, stream), h)
 
 
 def mtdao_read_state(h: int, state: int, replica: int, offset: int, count: int,

@@ -123,17 +123,24 @@ class MtdaoOptimizer:
         assert clip_table is None or (clip_table.dtype == torch.float32 and clip_table.numel() == lr_table.numel())
         # one block for the optimizer's life: captured graphs keep its address
         if getattr(self, "_dstep", None) is None:
-            self._dstep = torch.zeros(abi.MTDAO_DEVICE_STEP_BYTES // 4, dtype=torch.float32, device=self.x.device)
+            self._dstep = torch.zeros(abi.MTDAO_DEVICE_STEP_BYTES // 8, dtype=torch.int64, device=self.x.device)
         self._lr_table, self._clip_table = lr_table, clip_table
         abi.mtdao_device_step_set(self.handle, self._dstep.data_ptr(), self.step_count, _stream())
 
     def step_sync_device(self, grads: torch.Tensor, mask: int = abi.MTDAO_SYNC_AUTO) -> int:
         """step_sync whose eta_t, c_t and bias corrections come from the
-        device-side update number (see device_step)."""
+        device-side update number (see device_step); the k-th call since the
+        last device_step / device_step_advance performs update s + k."""
         assert grads.is_contiguous() and grads.shape == (self.K, self.P)
         clip = self._clip_table.data_ptr() if self._clip_table is not None else None
         return abi.mtdao_step_sync_device(self.handle, grads.data_ptr(), self._dstep.data_ptr(),
                                           self._lr_table.data_ptr(), clip, self._lr_table.numel(), mask, _stream())
+
+    def device_step_advance(self) -> None:
+        """Move the device-side update count on by the step_sync_device
+        calls since the last device_step or advance (capture it with the
+        window it closes)."""
+        abi.mtdao_device_step_advance(self.handle, self._dstep.data_ptr(), _stream())
 
     def sync(self, mask: int = abi.MTDAO_SYNC_AUTO) -> int:
         return abi.mtdao_sync(self.handle, mask, _stream())

@@ -28,7 +28,7 @@ def build() -> str:
     host_san = [a for f in SAN for a in ("-Xarch_host", f)]
     subprocess.run([HIPCC, "--offload-arch=gfx950", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops", "-O1", "-g", "-std=c++17", "-fPIC", "-shared",
                     "-fno-omit-frame-pointer", *host_san, "-I", os.path.join(ROOT, "include"),
-                    "-o", LIB, src], check=True)
+                    "-o", LIB, src, "-L/opt/rocm/lib", "-lrocprofiler-sdk-roctx", "-Wl,-rpath,/opt/rocm/lib"], check=True)
     subprocess.run([CLANG, "-O1", "-g", "-std=c11", "-fno-omit-frame-pointer", *SAN, "-I",
                     os.path.join(ROOT, "include"), "-o", BIN, os.path.join(HERE, "host_abi_check.c"), LIB,
                     "-Wl,-rpath," + HERE, "-L/opt/rocm/lib", "-lamdhip64", "-Wl,-rpath,/opt/rocm/lib"], check=True)

@@ -433,6 +433,10 @@ def test_device_step_host_rules():
             abi.mtdao_step_sync_device(h, g, 1 << 44, 1 << 45, None, 4, 1 << 5, None)
         assert e.value.code == abi.MTDAO_ERR_INVALID_ARG
         assert abi.mtdao_step_count(h) == 0
+        with pytest.raises(abi.MtdaoError) as e:
+            abi.mtdao_device_step_advance(h, (1 << 44) + 8, None)
+        assert e.value.code == abi.MTDAO_ERR_ALIGN
+        abi.mtdao_device_step_advance(h, 1 << 44, None)  # no calls since the last set: nothing enqueued
     finally:
         abi.mtdao_destroy(h)
     adopt = good_cfg(form="adopt", beta2=0.9999)
