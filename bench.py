@@ -316,6 +316,19 @@ def _event_times(fn, reps: int, stream) -> list:
     return [a.elapsed_time(b) for a, b in evs]
 
 
+def layout_json(opt, layout):
+    """Where the [K][P] buffers sit in the optimizer's allocation."""
+    names = ["x"] + (["g"] if opt.grad is not None else []) + [f"u{j + 1}" for j in range(opt.N)] \
+        + (["v"] if opt.has_v else [])
+    out = {"mode": layout, "order": [names[i] for i in opt.layout_order] if opt.layout_order else None}
+    r = opt.layout_report
+    if r is not None:
+        out.update({"candidates": r["candidates"], "packed_ms": r["packed_ms"], "best_ms": r["best_ms"],
+                    "worst_ms": r["worst_ms"],
+                    "note": "one timed pass of the local step per candidate order, over zeroed buffers"})
+    return out
+
+
 def device_info() -> dict:
     import torch
 
@@ -545,6 +558,10 @@ def main() -> int:
     ap.add_argument("--grad-in-arena", type=int, choices=[0, 1], default=1,
                     help="1: the gradient rows are carved from the optimizer's own allocation (default); "
                          "0: a separate torch allocation")
+    ap.add_argument("--layout", choices=["tuned", "packed"], default="tuned",
+                    help="order of x, the gradient rows, u^j and v in the optimizer's allocation: the "
+                         "fastest of a set of candidates timed at start-up (default), or the fixed order "
+                         "(--grad-in-arena 0 implies packed)")
     ap.add_argument("--row", choices=["step", "outer", "stats", "prob", "graph"], default="step",
                     help="step: the hot path (the default line); outer / stats / prob: the kernels of the "
                          "Nesterov OuterOpt, the averaging diagnostics, Algorithm 4's step (--steps = reps); "
@@ -581,7 +598,12 @@ def main() -> int:
           f"window s={start + args.warmup + 1}..{start + args.warmup + args.steps}", file=sys.stderr, flush=True)
     dev = DeviceInputs(w, d)
     cfg = abi.config_from_workload(w, start_step=start)
-    opt = MtdaoOptimizer(cfg, d, x0=dev.x0_row(), grad_buffer=bool(args.grad_in_arena))
+    layout = args.layout if args.grad_in_arena else "packed"
+    opt = MtdaoOptimizer(cfg, d, x0=dev.x0_row(), grad_buffer=bool(args.grad_in_arena), layout=layout)
+    if opt.layout_report is not None:
+        r = opt.layout_report
+        print(f"bench: layout tuned over {r['candidates']} orders: packed {r['packed_ms']:.4f} ms, "
+              f"best {r['best_ms']:.4f} ms, worst {r['worst_ms']:.4f} ms", file=sys.stderr, flush=True)
     if args.grad_in_arena:
         grads = opt.grad
     else:
@@ -646,6 +668,7 @@ def main() -> int:
     sync_s = []
     for sid in range(nstates):
         sync_s.append(_median(_event_times(lambda sid=sid: opt.sync(1 << sid), 20, stream)) / 1e3)
+    layout_info = layout_json(opt, layout)
     opt.close()
     del opt, grads
     torch.cuda.empty_cache()
@@ -705,7 +728,8 @@ def main() -> int:
                    "periods": {"x": w.period_x, "u": list(w.period_u), "v": w.period_v},
                    "window_steps": [start + args.warmup + 1, start + args.warmup + args.steps],
                    "syncs_in_window": {str(k): v for k, v in sorted(syncs.items())},
-                   "grad_in_arena": bool(args.grad_in_arena)},
+                   "grad_in_arena": bool(args.grad_in_arena),
+                   "layout": layout_info},
         "device": device_info(),
         "step": {"mean_launch_ms": step_launch_s * 1e3,
                  "median_launch_ms": _median(plain if plain else call_ms),

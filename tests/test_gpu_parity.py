@@ -8,6 +8,8 @@ and on the per-worker clip norms, which the oracle takes over full rows).
 The applied sync mask of every step must equal the oracle's bit for bit.
 """
 
+import math
+
 import numpy as np
 import pytest
 import torch
@@ -1080,3 +1082,30 @@ def test_long_run_within_tolerance(name, steps):
     assert g.masks == o.masks
     compare(w, g.opt, o, f"long-{name}")
     free(g)
+
+
+@pytest.mark.parametrize("name", ["adam_n3_k4_p16m", "adopt_n2_k8_p124m_bf16", "sgdm_n2_k16_p354m_clip"])
+def test_tuned_layout_same_results(name):
+    """The tuned arena layout only moves buffers: steps and averaging events
+    over it give bit-identical states to the packed layout, the chosen order
+    is a permutation of the [K][P] buffers, and the tuning passes left no
+    trace in the states (each optimizer starts from x_0 and zero moments)."""
+    w = synth.small_variant(synth.WORKLOADS[name], 40_000, tail=12)
+    w = w.replace(steps=20, period_x=4, period_u=(8,) * w.n_moments, period_v=16 if w.form != "sgdm" else 0)
+    log(f"case tuned-layout {w.name} K={w.replicas} P={w.numel}")
+    d = torch.device("cuda:0")
+    dev = DeviceInputs(w, d)
+    a = MtdaoOptimizer(abi.config_from_workload(w), d, x0=dev.x0_row(), grad_buffer=True)
+    b = MtdaoOptimizer(abi.config_from_workload(w), d, x0=dev.x0_row(), grad_buffer=True, layout="tuned")
+    n_rows = 3 + w.n_moments - (1 if w.form == "sgdm" else 0)
+    assert sorted(b.layout_order) == list(range(n_rows))
+    assert b.layout_report["candidates"] == min(24, math.factorial(n_rows))
+    for s in _steps(w):
+        dev.grads_into(s, a.grad)
+        b.grad.copy_(a.grad)
+        assert a.step_sync(a.grad, w.lr, w.adopt_clip_value(s)) == b.step_sync(b.grad, w.lr, w.adopt_clip_value(s))
+    torch.cuda.synchronize()
+    for p, q in zip(a.states(), b.states()):
+        assert torch.equal(p, q)
+    a.close()
+    b.close()
