@@ -43,7 +43,9 @@ def pytest_terminal_summary(terminalreporter, exitstatus, config):
             tr.write_line(label + ": " + " ".join(f"{k}={v:.2e}" for k, v in d.items()))
     tr.write_line("worst: " + " ".join(f"{k}={v:.2e}({lab})" for k, (v, lab) in sorted(worst.items())))
     out = os.path.join(ROOT, "gpurun_out")
-    if os.path.isdir(out):
+    # only GPU comparisons are written (the CPU suite compares the harness with itself)
+    if os.path.isdir(out) and any(not label.startswith("self") for label, _ in gh.REPORT) \
+            and "torch" in sys.modules and sys.modules["torch"].cuda.is_available():
         import json
         with open(os.path.join(out, "parity_report.jsonl"), "w") as f:
             for label, d in gh.REPORT:
