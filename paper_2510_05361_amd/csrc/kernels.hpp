@@ -44,6 +44,15 @@ __device__ __forceinline__ uint16_t f32_to_bf16(float f) {
   return (uint16_t)(u >> 16);
 }
 
+// A wave-uniform value that no running kernel writes (a parameter table, the
+// device-side step count, the clip factors of an earlier launch), read
+// through the scalar cache: the load waits only on other scalar loads,
+// never on the vector loads of the tile in flight.
+template <typename T>
+__device__ __forceinline__ T load_uniform(const T* p) {
+  return *(const __attribute__((address_space(4))) T*)p;
+}
+
 // --------------------------------------------------- vector load / store
 //
 // load_v<T, V>(p, e, out): V consecutive elements starting at element e,
@@ -303,25 +312,33 @@ struct StepParams {
   BiasCorrection bc;
 };
 
+// A value every lane of the wave holds, moved to a scalar register (the
+// fp64 arithmetic below runs in the vector ALU, whose results would
+// otherwise each hold a vector register for the rest of the kernel).
+__device__ __forceinline__ float wave_uniform(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_readfirstlane(__builtin_bit_cast(int, v)));
+}
+
 // The launch's scalars: those of the argument block, or those of the
 // device-side update number when it is given (every workgroup forms them;
-// a few dozen double multiplies).
+// a few dozen double multiplies).  Called where every lane of the wave is
+// active.
 __device__ __forceinline__ StepParams device_scalars(const StepParams& p0) {
 #pragma clang fp contract(off)
   if (p0.dev == nullptr) return p0;
   StepParams p = p0;
-  const int64_t s = p0.dev->s + p0.dev_k;
+  const int64_t s = load_uniform(&p0.dev->s) + p0.dev_k;
   const int64_t i = (s < p0.table_len ? s : p0.table_len) - 1;
-  p.lr = p0.lr_table[i];
-  p.clip = p0.clip_table != nullptr ? p0.clip_table[i] : 0.0f;
+  p.lr = load_uniform(p0.lr_table + i);
+  p.clip = p0.clip_table != nullptr ? load_uniform(p0.clip_table + i) : 0.0f;
   // step_scalars with the moment loop unrolled (a runtime-indexed store
   // would put the whole parameter block in private memory)
 #pragma unroll
   for (int j = 0; j < kMaxN; ++j)
     if (j < p0.bc.n)
-      p.w[j] = (float)(p0.bc.on ? (double)p0.bc.omega[j] / (1.0 - pow_steps((double)p0.bc.beta[j], s))
-                                : (double)p0.bc.omega[j]);
-  p.inv_bc2 = (float)(p0.bc.on ? 1.0 / (1.0 - pow_steps((double)p0.bc.beta2, s)) : 1.0);
+      p.w[j] = wave_uniform((float)(p0.bc.on ? (double)p0.bc.omega[j] / (1.0 - pow_steps((double)p0.bc.beta[j], s))
+                                             : (double)p0.bc.omega[j]));
+  p.inv_bc2 = wave_uniform((float)(p0.bc.on ? 1.0 / (1.0 - pow_steps((double)p0.bc.beta2, s)) : 1.0));
   return p;
 }
 
@@ -417,7 +434,7 @@ __global__ __launch_bounds__(B) void k_local_step(StepParams p0) {
 #pragma unroll
     for (int j = 0; j < N; ++j) u[j] = p0.u[j] + row;
     float* __restrict__ v = (FORM == kSgdm) ? nullptr : p0.v + row;
-    const float sc = (FORM != kAdopt && p0.scale != nullptr) ? p0.scale[m] : 1.0f;
+    const float sc = (FORM != kAdopt && p0.scale != nullptr) ? load_uniform(p0.scale + m) : 1.0f;
     float gv[U][V], xv[U][V], uv[U][N][V], vv[U][V];
     // issue every load of the tile before any arithmetic
 #pragma unroll
@@ -517,7 +534,7 @@ __global__ __launch_bounds__(kBlock) void k_local_step_sync(StepParams p0, uint3
 #pragma unroll
       for (int j = 0; j < N; ++j) load_v<float, V, NTL>(p.u[j], r, uv[j]);
       if constexpr (FORM != kSgdm) load_v<float, V, NTL>(p.v, r, vv);
-      const float sc = (FORM != kAdopt && p.scale != nullptr) ? p.scale[m] : 1.0f;
+      const float sc = (FORM != kAdopt && p.scale != nullptr) ? load_uniform(p.scale + m) : 1.0f;
 #pragma unroll
       for (int t = 0; t < V; ++t) {
         float uu[N];
@@ -605,13 +622,22 @@ template <int FORM, int N, typename XT, typename GT, int V, int NTM, int ORDER>
 __global__ __launch_bounds__(64 * kWaveMaxK) __attribute__((amdgpu_waves_per_eu(8)))
 void k_local_step_sync_waves(StepParams p0, uint32_t mask, int32_t K) {
   constexpr bool NTL = (NTM & 1) != 0, NTS = (NTM & 2) != 0;
+  // The device-side update number's scalars take a few dozen fp64
+  // operations.  Formed after a tile's loads are issued, their latency is
+  // hidden, but their temporaries meet the loaded values: with six or more
+  // streams loaded that exceeded the 64-register budget and spilled, so
+  // those forms take them once per workgroup before any load.
+  constexpr bool kEarly = 2 + N + (FORM != kSgdm ? 1 : 0) >= 6;
+  const StepParams early = kEarly ? device_scalars(p0) : p0;
   constexpr int NS = 2 + N;  // x, u^1..u^N, v
   __shared__ float lds[kWaveMaxK][64 * V];
   const int32_t m = threadIdx.x >> 6, lane = threadIdx.x & 63;
   XT* __restrict__ x = reinterpret_cast<XT*>(p0.x);
   const GT* __restrict__ g = reinterpret_cast<const GT*>(p0.g);
   const double rk = 1.0 / (double)K;
-  const float sc = (FORM != kAdopt && p0.scale != nullptr) ? p0.scale[m] : 1.0f;
+  // m is the same in every lane of a wave: readfirstlane makes that visible
+  const float sc =
+      (FORM != kAdopt && p0.scale != nullptr) ? load_uniform(p0.scale + __builtin_amdgcn_readfirstlane(m)) : 1.0f;
 
   for (int64_t tile = blockIdx.x; tile < p0.tiles; tile += gridDim.x) {
     const int64_t e = tile * (int64_t)(64 * V) + (int64_t)lane * V;
@@ -626,7 +652,7 @@ void k_local_step_sync_waves(StepParams p0, uint32_t mask, int32_t K) {
       for (int j = 0; j < N; ++j) load_v<float, V, NTL>(p0.u[j], r, uv[j]);
       if constexpr (FORM != kSgdm) load_v<float, V, NTL>(p0.v, r, val[NS - 1]);
       // the step-dependent scalars after the loads are in flight
-      const StepParams p = device_scalars(p0);
+      const StepParams p = kEarly ? early : device_scalars(p0);
 #pragma unroll
       for (int t = 0; t < V; ++t) {
         float uu[N];
@@ -716,7 +742,7 @@ __global__ __launch_bounds__(kBlock) void k_sgdm_averaged_momenta(StepParams p0,
       load_v<GT, V, NTL>(g, r, gv);
 #pragma unroll
       for (int j = 0; j < N; ++j) load_v<float, V, NTL>(p.u[j], r, uv[j]);
-      const float sc = p.scale != nullptr ? p.scale[m] : 1.0f;
+      const float sc = p.scale != nullptr ? load_uniform(p.scale + m) : 1.0f;
 #pragma unroll
       for (int t = 0; t < V; ++t) {
         const float gh = sc * gv[t];
@@ -762,7 +788,7 @@ __global__ __launch_bounds__(kBlock) void k_sgdm_averaged_momenta(StepParams p0,
           load_v<float, V, false>(p.u[j], r, uv[j]);
         }
       }
-      const float sc = p.scale != nullptr ? p.scale[m] : 1.0f;
+      const float sc = p.scale != nullptr ? load_uniform(p.scale + m) : 1.0f;
 #pragma unroll
       for (int t = 0; t < V; ++t) {
         const float gh = sc * gv[t];
@@ -809,7 +835,7 @@ void k_sgdm_averaged_momenta_waves(StepParams p0, uint32_t mask, int32_t K) {
   XT* __restrict__ x = reinterpret_cast<XT*>(p.x);
   const GT* __restrict__ g = reinterpret_cast<const GT*>(p.g);
   const double rk = 1.0 / (double)K;
-  const float sc = p.scale != nullptr ? p.scale[m] : 1.0f;
+  const float sc = p.scale != nullptr ? load_uniform(p.scale + __builtin_amdgcn_readfirstlane(m)) : 1.0f;
 
   // the mean over the replicas of val (this wave's row values), through
   // LDS, written back into val
