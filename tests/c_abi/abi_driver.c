@@ -15,6 +15,12 @@
  *           in the header's MTDAO_STAT_* layout) against the oracle's on
  *           the same pre-average states, within 1e-5 of
  *           max(|want|, 1e-6 * the largest statistic of the state).
+ *   case 4: Adam form with bias correction, N = 2, K = 3, P = 4100, through
+ *           a HIP graph: one window of 8 mtdao_step_sync_device calls (the
+ *           update number kept on the device, eta_t from a device table that
+ *           changes every step) and its mtdao_device_step_advance, captured
+ *           once and replayed 3 times, with new gradients written between
+ *           replays; the oracle runs the same 24 updates.
  * Every step's mask is also checked against mtdao_schedule (host only).
  * Inputs are seeded splitmix64 fields made here; the driver holds none of
  * the method's arithmetic.  Pass: every applied mask equals the oracle's
@@ -78,7 +84,11 @@ typedef struct {
   int64_t P;
   float beta1[4], omega[4], beta2, eps, rho, lr;
   int32_t period_x, period_u[4], period_v, steps, fused, stats;
+  int32_t graph; /* > 0: steps run as steps / graph replays of a captured window of this many calls */
 } drv_case;
+
+/* eta_t of the graph case: a ramp, so that every update takes its own value */
+static float ramp_lr(float lr, int64_t s) { return lr * (1.0f + 0.05f * (float)s); }
 
 static double compare(const float* a, const float* b, int64_t n) {
   double ss = 0.0, worst = 0.0;
@@ -175,7 +185,54 @@ static int run_case(const drv_case* t) {
   int masks_ok = 1;
   uint32_t nsync = 0;
 
+  /* graph case: capture one window, replay it; the oracle runs every update */
+  hipGraphExec_t gexec = NULL;
+  hipGraph_t graph = NULL;
+  mtdao_device_step* dstep = NULL;
+  float* dlr = NULL;
+  uint32_t captured[64];
+  const int32_t W = t->graph;
+  const int64_t table_len = 64;
+  if (W > 0) {
+    float lr_host[64];
+    for (int64_t i = 0; i < table_len; ++i) lr_host[i] = ramp_lr(t->lr, i + 1);
+    CHECK_HIP(hipMalloc((void**)&dstep, sizeof(mtdao_device_step)));
+    CHECK_HIP(hipMalloc((void**)&dlr, (size_t)table_len * 4));
+    CHECK_HIP(hipMemcpy(dlr, lr_host, (size_t)table_len * 4, hipMemcpyHostToDevice));
+    CHECK_MT(h, mtdao_device_step_set(h, dstep, 0, (void*)st));
+    CHECK_HIP(hipStreamSynchronize(st));
+    CHECK_HIP(hipStreamBeginCapture(st, hipStreamCaptureModeGlobal));
+    for (int32_t k = 0; k < W; ++k)
+      CHECK_MT(h, mtdao_step_sync_device(h, dg, dstep, dlr, NULL, table_len, MTDAO_SYNC_AUTO, &captured[k], (void*)st));
+    CHECK_MT(h, mtdao_device_step_advance(h, dstep, (void*)st));
+    CHECK_HIP(hipStreamEndCapture(st, &graph));
+    CHECK_HIP(hipGraphInstantiate(&gexec, graph, NULL, NULL, 0));
+  }
+
   for (int32_t s = 1; s <= t->steps; ++s) {
+    if (W > 0) {
+      /* one gradient per window, written between replays */
+      const int32_t win = (s - 1) / W, k = (s - 1) % W;
+      for (int32_t m = 0; m < K; ++m)
+        for (int64_t i = 0; i < P; ++i) g[(int64_t)m * P + i] = 1e-2f * field(5000 + 131 * (uint64_t)win + m, i);
+      if (k == 0) {
+        CHECK_HIP(hipMemcpyAsync(dg, g, (size_t)KP * 4, hipMemcpyHostToDevice, st));
+        CHECK_HIP(hipGraphLaunch(gexec, st));
+        CHECK_HIP(hipStreamSynchronize(st));
+      }
+      oracle_local_step(&oc, s, ramp_lr(t->lr, s), 0.0f, NULL, x, ou, v, g, K, P);
+      const uint32_t want = oracle_schedule(s, N, t->period_x, t->period_u, t->period_v, has_v);
+      if (want & 1u) oracle_replica_mean(x, 0, K, P);
+      for (int j = 0; j < N; ++j)
+        if (want & (1u << (j + 1))) oracle_replica_mean(u[j], 0, K, P);
+      if (has_v && (want & (1u << (N + 1)))) oracle_replica_mean(v, 0, K, P);
+      if (captured[k] != want) {
+        fprintf(stderr, "%s: step %d captured mask 0x%x, oracle 0x%x\n", t->name, s, captured[k], want);
+        masks_ok = 0;
+      }
+      nsync += (uint32_t)__builtin_popcount(want);
+      continue;
+    }
     for (int32_t m = 0; m < K; ++m)
       for (int64_t i = 0; i < P; ++i) g[(int64_t)m * P + i] = 1e-2f * field(1000 + 131 * (uint64_t)s + m, i);
     CHECK_HIP(hipMemcpyAsync(dg, g, (size_t)KP * 4, hipMemcpyHostToDevice, st));
@@ -252,8 +309,23 @@ static int run_case(const drv_case* t) {
     if (!(e <= worst)) worst = e;
   }
   const int64_t count = mtdao_step_count(h);
+  int64_t want_count = t->steps;
+  if (W > 0) {
+    /* the handle's host count moved during the capture only; the device count with every replay */
+    mtdao_device_step ds;
+    CHECK_HIP(hipMemcpy(&ds, dstep, sizeof ds, hipMemcpyDeviceToHost));
+    if (ds.s != t->steps) {
+      fprintf(stderr, "%s: device step count %lld, want %d\n", t->name, (long long)ds.s, t->steps);
+      masks_ok = 0;
+    }
+    want_count = W;
+    CHECK_HIP(hipGraphExecDestroy(gexec));
+    CHECK_HIP(hipGraphDestroy(graph));
+    CHECK_HIP(hipFree(dstep));
+    CHECK_HIP(hipFree(dlr));
+  }
   mtdao_destroy(h);
-  const int ok = masks_ok && worst <= 1e-5 && stats_worst <= 1e-5 && count == t->steps;
+  const int ok = masks_ok && worst <= 1e-5 && stats_worst <= 1e-5 && count == want_count;
   printf("%s: K=%d P=%lld N=%d steps=%d state-syncs=%u max rel err %.3e", t->name, K, (long long)P, N, t->steps,
          nsync, worst);
   if (t->stats) printf(" diagnostics err %.3e", stats_worst);
@@ -275,15 +347,17 @@ static int run_case(const drv_case* t) {
 }
 
 int main(void) {
-  const drv_case cases[3] = {
+  const drv_case cases[4] = {
       {"adam_n3_k4_step_sync", MTDAO_ADAM, 4, 3, 10007, {0.9f, 0.99f, 0.999f}, {0.3f, 0.3f, 0.3f}, 0.999f, 1e-8f,
-       0.0f, 1e-3f, 4, {8, 8, 16}, 16, 32, 1, 0},
+       0.0f, 1e-3f, 4, {8, 8, 16}, 16, 32, 1, 0, 0},
       {"sgdm_n2_k5_clip_sync", MTDAO_SGDM, 5, 2, 8204, {0.9f, 0.99f}, {0.3f, 0.6f}, 0.0f, 0.0f, 0.05f, 1e-2f, 4,
-       {2, 8}, 0, 24, 0, 0},
+       {2, 8}, 0, 24, 0, 0, 0},
       {"adam_n2_k6_sync_stats", MTDAO_ADAM, 6, 2, 4099, {0.9f, 0.99f}, {0.4f, 0.4f}, 0.999f, 1e-8f, 0.0f, 1e-3f, 4,
-       {0, 0}, 0, 6, 0, 1},
+       {0, 0}, 0, 6, 0, 1, 0},
+      {"adam_n2_k3_graph_device_step", MTDAO_ADAM, 3, 2, 4100, {0.9f, 0.99f}, {0.3f, 0.5f}, 0.999f, 1e-8f, 0.0f,
+       1e-3f, 4, {8, 8}, 8, 24, 1, 0, 8},
   };
   int all = 1;
-  for (int i = 0; i < 3; ++i) all &= run_case(&cases[i]);
+  for (int i = 0; i < 4; ++i) all &= run_case(&cases[i]);
   return all ? 0 : 1;
 }

@@ -3,8 +3,10 @@
 The driver allocates with hipMalloc, enqueues on a HIP stream of its own
 and has no Python or torch on its path.  It runs an Adam case through
 mtdao_step_sync, a clipped SGDM case through mtdao_local_step +
-mtdao_sync, and an Adam case that ends with mtdao_sync_stats of every
-state.  Every state it reads back through mtdao_read_state is checked
+mtdao_sync, an Adam case that ends with mtdao_sync_stats of every
+state, and an Adam case with bias correction and a per-step eta_t table
+whose window of mtdao_step_sync_device calls is captured into a HIP graph
+in C and replayed three times.  Every state it reads back through mtdao_read_state is checked
 against the CPU oracle on the same inputs, the diagnostics against the
 oracle's, and every applied mask and mtdao_schedule against the oracle's
 schedule.
@@ -41,9 +43,10 @@ def test_driver_links_the_in_tree_libraries():
 
 @pytest.mark.gpu
 def test_c_driver_matches_oracle():
-    print("c-abi driver: adam_n3_k4_step_sync, sgdm_n2_k5_clip_sync, adam_n2_k6_sync_stats", flush=True)
+    print("c-abi driver: adam_n3_k4_step_sync, sgdm_n2_k5_clip_sync, adam_n2_k6_sync_stats, "
+          "adam_n2_k3_graph_device_step", flush=True)
     r = subprocess.run([BIN], capture_output=True, text=True, timeout=180)
     print(r.stdout, r.stderr, flush=True)
     assert r.returncode == 0, r.stderr
     lines = [ln for ln in r.stdout.splitlines() if ln.strip()]
-    assert len(lines) == 3 and all(ln.endswith("-> ok") for ln in lines), r.stdout
+    assert len(lines) == 4 and all(ln.endswith("-> ok") for ln in lines), r.stdout
