@@ -23,7 +23,28 @@ BIN = os.path.join(HERE, "host_abi_check")
 SAN = ["-fsanitize=address", "-fsanitize=undefined"]
 
 
+STAMP = os.path.join(HERE, ".build_stamp")
+
+
+def _inputs_hash() -> str:
+    """Hash of everything the two outputs are built from (sources and this
+    script), so an unchanged tree reuses them."""
+    import hashlib
+    h = hashlib.sha256()
+    for f in (os.path.join(ROOT, "paper_2510_05361_amd", "csrc", "mtdao.hip"),
+              os.path.join(ROOT, "paper_2510_05361_amd", "csrc", "kernels.hpp"),
+              os.path.join(ROOT, "include", "mtdao.h"), os.path.join(HERE, "host_abi_check.c"), __file__):
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
 def build() -> str:
+    key = _inputs_hash()
+    if os.path.exists(LIB) and os.path.exists(BIN) and os.path.exists(STAMP):
+        with open(STAMP) as f:
+            if f.read().strip() == key:
+                return BIN
     src = os.path.join(ROOT, "paper_2510_05361_amd", "csrc", "mtdao.hip")
     host_san = [a for f in SAN for a in ("-Xarch_host", f)]
     subprocess.run([HIPCC, "--offload-arch=gfx950", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops", "-O1", "-g", "-std=c++17", "-fPIC", "-shared",
@@ -32,6 +53,8 @@ def build() -> str:
     subprocess.run([CLANG, "-O1", "-g", "-std=c11", "-fno-omit-frame-pointer", *SAN, "-I",
                     os.path.join(ROOT, "include"), "-o", BIN, os.path.join(HERE, "host_abi_check.c"), LIB,
                     "-Wl,-rpath," + HERE, "-L/opt/rocm/lib", "-lamdhip64", "-Wl,-rpath,/opt/rocm/lib"], check=True)
+    with open(STAMP, "w") as f:
+        f.write(key + "\n")
     return BIN
 
 
