@@ -108,6 +108,10 @@ DEVICE_CASES = {
     # clipped SGDM, K = 16 (wave-per-replica fused kernel), clip-norm pass inside the graph
     "sgdm_clip_k16": (synth.small_variant(synth.WORKLOADS["sgdm_n2_k16_p354m_clip"], 40_000, tail=37)
                       .replace(period_x=4, period_u=(2, 4)), 4),
+    # Adam N = 3 with bias correction, K = 4: six streams, so the fused kernel forms the
+    # device-side scalars once per workgroup before its loads (the other cases form them after)
+    "adam_n3_k4_early_scalars": (synth.small_variant(synth.WORKLOADS["adam_n3_k4_p16m"], 40_000, tail=13)
+                                 .replace(period_x=2, period_u=(4, 4, 4), period_v=4), 4),
 }
 
 
