@@ -112,18 +112,25 @@ DEVICE_CASES = {
     # device-side scalars once per workgroup before its loads (the other cases form them after)
     "adam_n3_k4_early_scalars": (synth.small_variant(synth.WORKLOADS["adam_n3_k4_p16m"], 40_000, tail=13)
                                  .replace(period_x=2, period_u=(4, 4, 4), period_v=4), 4),
+    # Algorithm 4's order (moments averaged inside the step), K = 5
+    "sgdm_momenta_in_step": (synth.small_variant(synth.WORKLOADS["sgdm_n2_k16_p354m_clip"], 30_000, tail=8)
+                             .replace(replicas=5, period_x=4, period_u=(2, 4)), 4,
+                             {"sync_order": abi.MTDAO_SYNC_MOMENTA_IN_STEP}),
+    # K = 17: the thread-per-column fused kernel
+    "adam_k17": (synth.small_variant(synth.WORKLOADS["adam_n2_k2_p1m"], 20_000, tail=8)
+                 .replace(replicas=17, period_x=4, period_u=(8, 8), period_v=8), 8),
 }
 
 
 @pytest.mark.parametrize("case", sorted(DEVICE_CASES))
 def test_graph_device_step_equals_eager(case):
-    w, window = DEVICE_CASES[case]
+    w, window, *extra = DEVICE_CASES[case]
     replays = 3
     n_total = 1 + window * (replays + 1)
     log(f"case graph device step {case} P={w.numel} K={w.replicas} window={window}")
     d = torch.device("cuda:0")
     dev = DeviceInputs(w, d)
-    cfg = abi.config_from_workload(w)
+    cfg = abi.config_from_workload(w, **(extra[0] if extra else {}))
     g_opt = MtdaoOptimizer(cfg, d, x0=dev.x0_row())
     e_opt = MtdaoOptimizer(cfg, d, x0=dev.x0_row())
     gdt = torch.bfloat16 if w.grad_dtype == "bf16" else torch.float32
