@@ -7,6 +7,8 @@ the library's kernels through the C ABI (``mtdao.py``).
 
 from __future__ import annotations
 
+import itertools
+import random
 from typing import List, Optional
 
 import torch
@@ -134,8 +136,6 @@ class MtdaoOptimizer:
         local step over zeroed buffers through a handle that keeps the
         states as they are (no initialisation pass): two untimed calls, then
         enough timed calls for about 0.1 s of work."""
-        import itertools
-        import random
         n = len(rows)
         orders = list(itertools.permutations(range(n)))
         if len(orders) > max_candidates:
