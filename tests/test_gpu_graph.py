@@ -119,6 +119,14 @@ DEVICE_CASES = {
     # K = 17: the thread-per-column fused kernel
     "adam_k17": (synth.small_variant(synth.WORKLOADS["adam_n2_k2_p1m"], 20_000, tail=8)
                  .replace(replicas=17, period_x=4, period_u=(8, 8), period_v=8), 8),
+    # Nesterov OuterOpt at every x averaging (the outer step of each replayed s runs once)
+    "adam_nesterov": (synth.small_variant(synth.WORKLOADS["adam_n2_k2_p1m"], 30_000, tail=12)
+                      .replace(replicas=4, period_x=2, period_u=(4, 4), period_v=4), 4,
+                      {"outer_opt": abi.MTDAO_OUTER_NESTEROV, "outer_lr": 0.7, "outer_momentum": 0.9}),
+    # one worker: the plain step over the row's two halves, an outer step only at x events
+    "adam_k1_nesterov": (synth.small_variant(synth.WORKLOADS["adam_n2_k2_p1m"], 30_000, tail=12)
+                         .replace(replicas=1, period_x=2, period_u=(4, 4), period_v=4), 4,
+                         {"outer_opt": abi.MTDAO_OUTER_NESTEROV, "outer_lr": 0.7, "outer_momentum": 0.9}),
 }
 
 
@@ -165,6 +173,8 @@ def test_graph_device_step_equals_eager(case):
         torch.cuda.synchronize()
         for k, (a, b) in enumerate(zip(g_opt.states(), e_opt.states())):
             assert torch.equal(a, b), f"replay {r}: state {k} differs"
+        if g_opt.x_outer is not None:
+            assert torch.equal(g_opt.x_outer, e_opt.x_outer) and torch.equal(g_opt.x_outer_mom, e_opt.x_outer_mom)
         assert int(g_opt._dstep[0].item()) == s
         log(f"  replay {r}: steps up to {s}, every state bit-identical to eager")
     del graph
