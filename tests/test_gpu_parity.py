@@ -343,38 +343,83 @@ def test_deterministic():
     free(a, b)
 
 
-def test_guard_bands_untouched():
-    """Canary regions around every buffer (states, gradients, workspace)
-    keep their contents through init, steps and syncs."""
-    w = synth.small_variant(synth.WORKLOADS["sgdm_n2_k16_p354m_clip"], 30_000, tail=37).replace(
-        replicas=5, steps=40, period_x=3, period_u=(2, 5))
+GUARD_CASES = {
+    # clipped SGDM, separate step and sync: the norm pass, the clip finalize, the mean
+    "sgdm_k5_clip_separate": (synth.small_variant(synth.WORKLOADS["sgdm_n2_k16_p354m_clip"], 30_000, tail=37)
+                              .replace(replicas=5, steps=40, period_x=3, period_u=(2, 5)), {}, False, False),
+    # Adam N = 3, fused step + sync with the Nesterov OuterOpt, then the diagnostics of every state
+    "adam_n3_k4_fused_nesterov_stats": (synth.small_variant(synth.WORKLOADS["adam_n3_k4_p16m"], 30_000, tail=13)
+                                        .replace(steps=24, period_x=2, period_u=(4, 4, 8), period_v=8),
+                                        {"outer_opt": abi.MTDAO_OUTER_NESTEROV, "outer_lr": 0.7,
+                                         "outer_momentum": 0.9}, True, True),
+    # ADOPT with bf16 x and g, fused, then the diagnostics (the bf16 x launch included)
+    "adopt_bf16_k8_fused_stats": (synth.small_variant(synth.WORKLOADS["adopt_n2_k8_p124m_bf16"], 30_000, tail=8)
+                                  .replace(steps=16, period_x=2, period_u=(4, 4), period_v=4), {}, True, True),
+    # Algorithm 4's order
+    "sgdm_k5_momenta_in_step": (synth.small_variant(synth.WORKLOADS["sgdm_n2_k16_p354m_clip"], 30_000, tail=5)
+                                .replace(replicas=5, steps=24, period_x=3, period_u=(2, 4)),
+                                {"sync_order": abi.MTDAO_SYNC_MOMENTA_IN_STEP}, True, False),
+    # K = 17: the thread-per-column fused kernel and mean
+    "adam_k17_fused": (synth.small_variant(synth.WORKLOADS["adam_n2_k2_p1m"], 20_000, tail=8)
+                       .replace(replicas=17, steps=16, period_x=2, period_u=(4, 4), period_v=8), {}, True, False),
+}
+
+
+@pytest.mark.parametrize("case", sorted(GUARD_CASES))
+def test_guard_bands_untouched(case):
+    """Canary regions around every buffer the library is given (states,
+    gradients, workspace, the outer parameters and momentum, the
+    diagnostics scratch) keep their contents through init, steps, syncs and
+    the diagnostics: no kernel writes outside its buffers."""
+    w, kw, fused, stats = GUARD_CASES[case]
+    log(f"case guard bands {case} K={w.replicas} P={w.numel}")
     d = torch.device("cuda:0")
     K, P, pad = w.replicas, w.numel, 4096
-    canary = float.fromhex("0x1.5555p-3")
+    cfg = abi.config_from_workload(w, **kw)
+    st = torch.cuda.current_stream().cuda_stream
+    canary32 = float.fromhex("0x1.5555p-3")
+    guards = []
 
-    def guarded(dtype):
-        big = torch.full((K * P + 2 * pad,), canary, dtype=dtype, device=d)
-        return big, big[pad:pad + K * P].view(K, P)
+    def guarded(n, dtype):
+        fill = 0xA5 if dtype == torch.uint8 else canary32
+        big = torch.full((n + 2 * pad,), fill, dtype=dtype, device=d)
+        guards.append((big, n, big[0].clone()))
+        return big[pad:pad + n]
 
-    bx, x = guarded(torch.float32)
-    bu = [guarded(torch.float32) for _ in range(2)]
-    bg, grads = guarded(torch.float32)
+    xdt = torch.bfloat16 if w.param_dtype == "bf16" else torch.float32
+    gdt = torch.bfloat16 if w.grad_dtype == "bf16" else torch.float32
+    x = guarded(K * P, xdt).view(K, P)
+    u = [guarded(K * P, torch.float32).view(K, P) for _ in range(w.n_moments)]
+    v = guarded(K * P, torch.float32).view(K, P) if w.form != "sgdm" else None
+    grads = guarded(K * P, gdt).view(K, P)
+    nesterov = kw.get("outer_opt") == abi.MTDAO_OUTER_NESTEROV
+    xo = guarded(P, torch.float32) if nesterov else None
+    mom = guarded(P, torch.float32) if nesterov else None
     dev = DeviceInputs(w, d)
-    x[0].copy_(dev.x0_row())
-    cfg = abi.config_from_workload(w)
+    x[0].copy_(dev.x0_row().to(xdt))
     ws_bytes = abi.mtdao_workspace_bytes(cfg)
-    wsbig = torch.full((ws_bytes + 2 * 4096,), 0xA5, dtype=torch.uint8, device=d)
-    bufs = abi.make_buffers(x.data_ptr(), [t.data_ptr() for _, t in bu], None, False)
-    h = abi.mtdao_init(cfg, bufs, wsbig[4096:].data_ptr(), ws_bytes, torch.cuda.current_stream().cuda_stream)
-    for s in range(1, w.steps + 1):
-        dev.grads_into(s, grads)
-        abi.mtdao_local_step(h, grads.data_ptr(), w.lr, 0.0, torch.cuda.current_stream().cuda_stream)
-        abi.mtdao_sync(h, abi.MTDAO_SYNC_AUTO, torch.cuda.current_stream().cuda_stream)
-    torch.cuda.synchronize()
-    for big in [bx, bg] + [b for b, _ in bu]:
-        assert torch.all(big[:pad] == canary) and torch.all(big[pad + K * P:] == canary)
-    assert torch.all(wsbig[:4096] == 0xA5) and torch.all(wsbig[4096 + ws_bytes:] == 0xA5)
-    abi.mtdao_destroy(h)
+    ws = guarded(max(ws_bytes, 256), torch.uint8)
+    bufs = abi.make_buffers(x.data_ptr(), [t.data_ptr() for t in u], v.data_ptr() if v is not None else None, False,
+                            xo.data_ptr() if nesterov else None, mom.data_ptr() if nesterov else None)
+    h = abi.mtdao_init(cfg, bufs, ws.data_ptr(), ws_bytes, st)
+    try:
+        for s_ in range(1, w.steps + 1):
+            dev.grads_into(s_, grads)
+            if fused:
+                abi.mtdao_step_sync(h, grads.data_ptr(), w.lr, w.adopt_clip_value(s_), abi.MTDAO_SYNC_AUTO, st)
+            else:
+                abi.mtdao_local_step(h, grads.data_ptr(), w.lr, w.adopt_clip_value(s_), st)
+                abi.mtdao_sync(h, abi.MTDAO_SYNC_AUTO, st)
+        if stats:
+            nbytes = abi.mtdao_stats_scratch_bytes(cfg)
+            scratch = guarded(nbytes, torch.uint8)
+            nstates = 2 + w.n_moments - (1 if w.form == "sgdm" else 0)
+            abi.mtdao_sync_stats(h, (1 << nstates) - 1, scratch.data_ptr(), nbytes, st)
+        torch.cuda.synchronize()
+        for k, (big, n, fill) in enumerate(guards):
+            assert torch.all(big[:pad] == fill) and torch.all(big[pad + n:] == fill), f"guard {k} written"
+    finally:
+        abi.mtdao_destroy(h)
 
 
 def test_row_longer_than_2_pow_31():
