@@ -254,7 +254,10 @@ int32_t mtdao_device_step_set(mtdao_handle* h, mtdao_device_step* d, int64_t s, 
  * eta_t = lr_table[s - 1] and c_t = clip_table[s - 1] (or off when
  * clip_table is NULL; the last entries for s > table_len) and the bias
  * corrections of Algorithm 1 formed from this s by the kernels.  The
- * tables are caller-owned device fp32 arrays.  Results equal
+ * tables are caller-owned device fp32 arrays; the kernels read them (and
+ * d) as constants, so they must not be written while a launch of this
+ * call runs (writes enqueued on the same stream before or after are
+ * ordered with it).  Results equal
  * mtdao_step_sync's with the same eta_t and c_t, bit for bit (the scalars
  * are formed by the same code on host and device).  k, the mask
  * (MTDAO_SYNC_AUTO: the schedule at the handle's step count + 1) and the
