@@ -68,3 +68,32 @@ def test_more_than_one_gpu_is_refused():
                        text=True, timeout=300, cwd=ROOT)
     assert r.returncode == 2
     assert "one GPU" in r.stderr and r.stdout.strip() == ""
+
+
+def test_arena_carving_orders():
+    """The optimizer's allocation (on the CPU here): every [K][P] buffer and
+    the tail buffers are disjoint, 256-byte aligned, of the requested shape
+    and type, laid out in the requested order, and returned in their own
+    order whatever the layout."""
+    import itertools
+
+    import torch
+
+    from paper_2510_05361_amd.optimizer import MtdaoOptimizer
+
+    K, P = 3, 1001
+    rows = [((K, P), torch.bfloat16), ((K, P), torch.bfloat16), ((K, P), torch.float32), ((K, P), torch.float32)]
+    tail = [((P,), torch.float32)] * 2
+    for order in itertools.permutations(range(len(rows))):
+        opt = object.__new__(MtdaoOptimizer)
+        opt._arena = None
+        views = opt._carve(rows, tail, list(order), torch.device("cpu"))
+        base = opt._arena.data_ptr()
+        assert len(views) == len(rows) + len(tail)
+        for v, (shape, dt) in zip(views, rows + tail):
+            assert tuple(v.shape) == shape and v.dtype == dt and (v.data_ptr() - base) % 256 == 0
+        spans = sorted((v.data_ptr(), v.data_ptr() + v.numel() * v.element_size()) for v in views)
+        assert all(a[1] <= b[0] for a, b in zip(spans, spans[1:]))
+        starts = [views[i].data_ptr() for i in order]
+        assert starts == sorted(starts)
+        assert min(v.data_ptr() for v in views[len(rows):]) > max(starts)
